@@ -1,0 +1,158 @@
+"""Seeded synthetic inputs for one draft-tree round.
+
+This module draws the tensors a tree-build round consumes: shared base logits
+``L[R][B][V]`` (standing in for one parallel-backbone forward, Sec. 3.2), the
+Markov-head parameters ``E[V][r]``, ``W[r][V]`` and per-depth features
+``h[R][B][r]``, the root token ``x_t`` and the verified-prefix length of each
+request.  It performs none of the method's arithmetic: it only draws numbers
+and rounds them once to the storage precision, so both the CPU oracle and the
+GPU path receive bit-identical operands.
+
+Recipe (the paper measured Qwen3-4B/8B/14B with DSpark drafts on nine public
+suites; none of those checkpoints or datasets are used, these seeded tensors
+stand in for them):
+
+* ``L_d[v] ~ N(0, 3^2)`` plus a peak added to 3 distinct tokens per depth whose
+  rank follows a Zipf(1.1) law truncated to ``[1, V]`` (token = rank - 1).
+  Peak height: +8 (``"const8"``), ``U(4, 12)`` per depth (``"uniform"``), or
+  ``12 - 9 d / (B - 1)`` (``"decay"``: confidence falling with depth).
+* ``E ~ N(0, 0.02)``, ``W ~ N(0, 0.05)`` (standard deviations), ``h ~ N(0, 1)``.
+* root token uniform over the vocabulary; prefix length uniform in [1, 1024].
+* Values are drawn in float64 and rounded once, round-to-nearest-even, to the
+  storage dtype (``"f32"`` or ``"bf16"``).  ``h`` is always float32.
+
+Streams: request ``i`` of a batch draws ``root, prefix_len, L, h`` from
+``default_rng((seed + i, 1))``; the shared head ``E, W`` comes from
+``default_rng((seed, 2))`` (one drafter serves every request).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+__all__ = ["Workload", "CONFIGS", "make_inputs", "round_to_bf16", "bf16_bits"]
+
+
+@dataclass(frozen=True)
+class Workload:
+    """Shape of one tree-build round (symbols as in the paper's Sec. 4.1)."""
+
+    name: str
+    V: int  # vocabulary size
+    B: int  # block size = number of sequential Markov stages
+    N: int  # verification node budget (root included)
+    k: int  # local branching factor
+    r: int  # Markov-head rank
+    R: int = 1  # independent requests built in one call
+    dtype: str = "bf16"  # storage dtype of L, E, W
+    peak: str = "const8"  # peak-height schedule of the base logits
+    seed: int = 0
+    sigma_L: float = 3.0
+    sigma_E: float = 0.02
+    sigma_W: float = 0.05
+    extra: dict = field(default_factory=dict)
+
+
+# The five workloads of the headline table plus the brute-force shape.
+CONFIGS = {
+    "tiny": Workload("tiny", V=1024, B=4, N=16, k=4, r=32, dtype="f32", peak="const8"),
+    "brute": Workload("brute", V=8, B=4, N=10, k=8, r=32, dtype="f32", peak="const8"),
+    "qwen4b_b7": Workload("qwen4b_b7", V=151936, B=7, N=32, k=8, r=256, peak="const8"),
+    "qwen8b_b7": Workload("qwen8b_b7", V=151936, B=7, N=48, k=8, r=384, peak="uniform"),
+    "qwen4b_b16": Workload("qwen4b_b16", V=151936, B=16, N=64, k=8, r=256, peak="decay"),
+    "qwen14b_b16_r8": Workload(
+        "qwen14b_b16_r8", V=151936, B=16, N=128, k=16, r=512, R=8, peak="decay"
+    ),
+}
+
+
+def round_to_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float64 values once, to nearest-even, onto the bfloat16 grid.
+
+    Returns float32 values that are exactly representable in bfloat16.
+    (Finite, normal-range inputs only; the generator never produces others.)
+    """
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)  # x = m * 2**e with 0.5 <= |m| < 1
+    q = np.rint(m * 256.0)  # 8 significant bits, ties to even
+    return np.ldexp(q / 256.0, e).astype(np.float32)
+
+
+def bf16_bits(x32: np.ndarray) -> np.ndarray:
+    """Upper 16 bits of float32 values that already lie on the bf16 grid."""
+    b = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32)
+    if np.any(b & 0xFFFF):
+        raise ValueError("values are not bfloat16-representable")
+    return (b >> 16).astype(np.uint16)
+
+
+def _round(x: np.ndarray, dtype: str) -> np.ndarray:
+    if dtype == "f32":
+        return x.astype(np.float32)
+    if dtype == "bf16":
+        return round_to_bf16(x)
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+def _zipf_tokens(rng: np.random.Generator, V: int, count: int, a: float = 1.1) -> np.ndarray:
+    """``count`` distinct tokens whose rank follows Zipf(a) truncated to [1, V]."""
+    count = min(count, V)
+    w = np.arange(1, V + 1, dtype=np.float64) ** (-a)
+    cdf = np.cumsum(w)
+    cdf /= cdf[-1]
+    out: list[int] = []
+    while len(out) < count:
+        t = int(np.searchsorted(cdf, rng.random(), side="right"))
+        t = min(t, V - 1)
+        if t not in out:
+            out.append(t)
+    return np.array(out, dtype=np.int64)
+
+
+def _peak_height(w: Workload, d: int, rng: np.random.Generator) -> float:
+    if w.peak == "const8":
+        return 8.0
+    if w.peak == "uniform":
+        return float(rng.uniform(4.0, 12.0))
+    if w.peak == "decay":
+        return 12.0 - 9.0 * d / max(w.B - 1, 1)
+    if w.peak == "none":
+        return 0.0
+    raise ValueError(f"unknown peak schedule {w.peak!r}")
+
+
+def make_inputs(w: Workload) -> dict:
+    """Draw one round's inputs.
+
+    Returns a dict of numpy arrays: ``L [R][B][V]``, ``E [V][r]``, ``W [r][V]``
+    (float32 holding values of the storage dtype), ``h [R][B][r]`` float32,
+    ``root [R]`` and ``prefix_len [R]`` int32, and ``workload``.
+    """
+    R, B, V, r = w.R, w.B, w.V, w.r
+    L = np.empty((R, B, V), dtype=np.float32)
+    h = np.empty((R, B, r), dtype=np.float32)
+    root = np.empty(R, dtype=np.int32)
+    prefix_len = np.empty(R, dtype=np.int32)
+    for i in range(R):
+        rng = np.random.default_rng((w.seed + i, 1))
+        root[i] = rng.integers(0, V)
+        prefix_len[i] = rng.integers(1, 1025)
+        Li = rng.standard_normal((B, V)) * w.sigma_L
+        for d in range(B):
+            toks = _zipf_tokens(rng, V, 3)
+            Li[d, toks] += _peak_height(w, d, rng)
+        L[i] = _round(Li, w.dtype)
+        h[i] = rng.standard_normal((B, r)).astype(np.float32)
+    rs = np.random.default_rng((w.seed, 2))
+    E = _round(rs.standard_normal((V, r)) * w.sigma_E, w.dtype)
+    W = _round(rs.standard_normal((r, V)) * w.sigma_W, w.dtype)
+    return {
+        "L": L,
+        "E": E,
+        "W": W,
+        "h": h,
+        "root": root,
+        "prefix_len": prefix_len,
+        "workload": w,
+    }
