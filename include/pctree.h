@@ -1,0 +1,164 @@
+/*
+ * pctree.h -- C ABI of the PCTree per-round draft-tree builder for MI355X (gfx950).
+ *
+ * One speculative-decoding round of PCTree (Li et al., "From Chains to Trees:
+ * Parent-Conditioned Drafting for Semi-Autoregressive Speculative Decoding")
+ * turns shared backbone logits L_0..L_{B-1} into a budgeted draft tree:
+ *
+ *   for every depth d (Sec. 4.1, Alg. 1): the frontier parents are batched
+ *   through the Markov head, z_d(p) = L_d + Markov(p) (Eq. 3), each row is
+ *   log-softmax normalised (Eq. 2), every parent keeps its top-k children with
+ *   joint path scores s(child) = s(p) + log pi_d(child|p) (Eq. 4), and the k
+ *   best candidates of the layer become the next frontier; after B stages the
+ *   global top-N of the pool (score desc, depth asc, stable id; Sec. 4.2) is
+ *   emitted as flat tokens, parent indices, position ids and the ancestor-only
+ *   tree attention mask (App. A).
+ *
+ * The Markov head is Markov_d(p) = W^T . SiLU(E[p] + h_d) with E[V][r],
+ * W[r][V] and a per-depth feature h_d[r]; the paper gives only that the head
+ * is low-rank and adds a bias set by the preceding token (Sec. 3.2).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every data pointer is a DEVICE pointer on the current HIP device; the
+ *    caller owns all memory, the library never allocates or frees.  Inputs
+ *    are never written.  Outputs must not overlap inputs or the workspace.
+ *  - Data pointers must be 16-byte aligned; the workspace 256-byte aligned.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Calls only
+ *    enqueue work: they return before the GPU has run it, do no host<->device
+ *    copies and never synchronise.  Results are valid once the stream reaches
+ *    that point.  Calls are re-entrant; concurrent calls need distinct
+ *    workspaces.
+ *  - Argument checking happens on the host before anything is enqueued; on
+ *    any error status no device work has been issued and nothing is written.
+ *    No C++ exception crosses this interface.
+ *  - Device-side data errors do not fault: a request whose root token lies
+ *    outside [0, V) is emitted as an empty tree (count = 0, rows padded).
+ *    Floating-point inputs must be finite.
+ */
+#ifndef PCTREE_H
+#define PCTREE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PCTREE_ABI_VERSION 1
+
+/* Compiled limits (PCTREE_ERR_UNSUPPORTED beyond them). */
+#define PCTREE_MAX_VOCAB (1 << 20)
+#define PCTREE_MAX_BLOCK 63
+#define PCTREE_MAX_TOPK 16
+#define PCTREE_MAX_BUDGET 256
+#define PCTREE_MAX_REQUESTS 256
+#define PCTREE_MAX_RANK_BF16 512 /* and rank % 32 == 0 */
+#define PCTREE_MAX_RANK_F32 128  /* and rank % 16 == 0 */
+#define PCTREE_MAX_MASK_BUDGET 1024
+
+typedef enum pctree_status {
+  PCTREE_OK = 0,
+  PCTREE_ERR_INVALID_ARGUMENT = 1, /* null pointer, size < 1, bad dtype, misaligned pointer */
+  PCTREE_ERR_UNSUPPORTED = 2,      /* beyond the compiled limits, or mode != 0 */
+  PCTREE_ERR_WORKSPACE = 3,        /* workspace null, too small or not 256-byte aligned */
+  PCTREE_ERR_HIP = 4               /* a kernel launch failed */
+} pctree_status;
+
+typedef enum pctree_dtype {
+  PCTREE_F32 = 0, /* float32 base logits and head weights */
+  PCTREE_BF16 = 1 /* bfloat16 base logits and head weights, fp32 accumulation */
+} pctree_dtype;
+
+/* Problem size of one round (symbols of Sec. 4.1). */
+typedef struct pctree_shape {
+  int32_t vocab;    /* V: vocabulary size                                    */
+  int32_t block;    /* B: block size = number of sequential Markov stages    */
+  int32_t budget;   /* N: verification node budget, root included            */
+  int32_t topk;     /* k: local branching factor (k' = min(k, V) is used)    */
+  int32_t rank;     /* r: Markov-head rank                                   */
+  int32_t requests; /* R: independent requests built in one call             */
+  int32_t dtype;    /* pctree_dtype of base_logits, emb and proj_t           */
+  int32_t mode;     /* 0 = parent-conditioned (PCTree); other values: UNSUPPORTED */
+} pctree_shape;
+
+/* Inputs of one round.  Request i uses base_logits[i], depth_feat[i],
+ * root_token[i] and prefix_len[i]; emb and proj_t are one drafter's head,
+ * shared by every request. */
+typedef struct pctree_inputs {
+  const void* base_logits;   /* L   [R][B][V] dtype: backbone logits L_d (Sec. 3.2)      */
+  const void* emb;           /* E   [V][r] dtype: parent-token embedding of the head     */
+  const void* proj_t;        /* W^T [V][r] dtype: proj_t[v*r + j] = W[j][v]              */
+  const float* depth_feat;   /* h   [R][B][r] float32: per-depth head feature            */
+  const int32_t* root_token; /* x_t [R]: last verified token, root of the tree           */
+  const int32_t* prefix_len; /* [R]: verified-prefix length; position = prefix + depth   */
+} pctree_inputs;
+
+/* The emitted tree (Sec. 4.2, App. A).  Nodes are in canonical order: depth
+ * ascending, then root-to-node token path lexicographically ascending, so
+ * node 0 is the root (token x_t, parent -1, depth 0, logprob 0) and
+ * parent[i] < i.  Rows i >= count[r] are padded with token = parent = depth =
+ * position = -1 and logprob = -inf (mask rows: zero words). */
+typedef struct pctree_tree {
+  int32_t* token;    /* [R][N] draft token ids                                   */
+  int32_t* parent;   /* [R][N] index of the parent node in the same row, -1 root */
+  int32_t* depth;    /* [R][N] tree depth (root 0)                               */
+  int32_t* position; /* [R][N] prefix_len + depth                                */
+  float* logprob;    /* [R][N] joint path score s(c) (Eq. 4), root 0             */
+  int32_t* count;    /* [R]    min(N, pool size)                                 */
+  uint32_t* mask;    /* optional (may be NULL): [R][N][(N+31)/32] ancestor mask,
+                        bit j%32 of word j/32 of row i is set iff node j is node
+                        i or one of its ancestors (same layout as build_mask)    */
+} pctree_tree;
+
+/* Optional per-stage record of the frontier (Alg. 1), for inspection.
+ * Entry [r][d][s] describes frontier slot s used at stage d: its token, the
+ * slot of its own parent in the frontier of stage d-1 (-1 for the root) and
+ * its joint score.  Stage 0 holds the root only.  Unused slots hold
+ * (-1, -1, -inf). */
+typedef struct pctree_trace {
+  int32_t* token;       /* [R][B][k] */
+  int32_t* parent_slot; /* [R][B][k] */
+  float* score;         /* [R][B][k] */
+} pctree_trace;
+
+/* Bytes of workspace that pctree_build_tree and pctree_chain_decode need for
+ * `shape` (0 if the shape is invalid or unsupported).  Pure host arithmetic. */
+size_t pctree_workspace_bytes(const pctree_shape* shape);
+
+/* Build one round's draft tree for every request (Alg. 1, Eq. 2-4, Sec. 4.2,
+ * App. A).  `trace` may be NULL.  The workspace's contents on entry do not
+ * matter; on return it holds scratch the caller must not rely on. */
+pctree_status pctree_build_tree(const pctree_shape* shape, const pctree_inputs* in,
+                                const pctree_tree* out, const pctree_trace* trace,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Ancestor-only tree attention mask from parent indices (App. A): row i of
+ * request r admits node i and its ancestors.  parent [R][N], count [R] (as
+ * emitted by pctree_build_tree), mask [R][N][(N+31)/32] uint32.  Rows at or
+ * beyond count are zero.  A parent index that is not in [-1, i) ends that
+ * row's walk.  Limits: N <= PCTREE_MAX_MASK_BUDGET. */
+pctree_status pctree_build_mask(const int32_t* parent, const int32_t* count, int32_t requests,
+                                int32_t budget, uint32_t* mask, void* stream);
+
+/* The DSpark greedy chain of Eq. 1: y_{-1} = x_t, y_d = argmax_v z_d(y_{d-1})
+ * (ties to the lowest token id).  Uses vocab, block, rank, requests, dtype and
+ * mode of `shape` (topk and budget are ignored).  chain_token [R][B+1] gets
+ * x_t, y_0..y_{B-1}; chain_logprob [R][B+1] the cumulative log-probabilities
+ * (0 for x_t).  Same workspace as pctree_build_tree. */
+pctree_status pctree_chain_decode(const pctree_shape* shape, const pctree_inputs* in,
+                                  int32_t* chain_token, float* chain_logprob, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/* Static, human-readable name of a status code. */
+const char* pctree_status_string(pctree_status status);
+
+/* PCTREE_ABI_VERSION of the loaded library. */
+int32_t pctree_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PCTREE_H */

@@ -1,0 +1,259 @@
+// C ABI of the PCTree tree builder: argument checking, workspace layout and
+// the launch sequence.  Every check runs on the host before anything is
+// enqueued, so an error status means no device work was issued.
+#include "pctree.h"
+
+#include <algorithm>
+
+#include "pctree_plan.h"
+
+namespace pctree {
+
+namespace {
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int pow2ceil(int x) {
+  int p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+bool aligned(const void* ptr, size_t a) { return ((uintptr_t)ptr & (a - 1)) == 0; }
+
+pctree_status check_shape(const pctree_shape* s) {
+  if (!s) return PCTREE_ERR_INVALID_ARGUMENT;
+  if (s->vocab < 1 || s->block < 1 || s->budget < 1 || s->topk < 1 || s->rank < 1 ||
+      s->requests < 1)
+    return PCTREE_ERR_INVALID_ARGUMENT;
+  if (s->dtype != PCTREE_F32 && s->dtype != PCTREE_BF16) return PCTREE_ERR_INVALID_ARGUMENT;
+  if (s->mode != 0) return PCTREE_ERR_UNSUPPORTED;
+  if (s->vocab > PCTREE_MAX_VOCAB || s->block > PCTREE_MAX_BLOCK || s->topk > PCTREE_MAX_TOPK ||
+      s->budget > PCTREE_MAX_BUDGET || s->requests > PCTREE_MAX_REQUESTS)
+    return PCTREE_ERR_UNSUPPORTED;
+  if (s->dtype == PCTREE_BF16 && (s->rank % 32 != 0 || s->rank > PCTREE_MAX_RANK_BF16))
+    return PCTREE_ERR_UNSUPPORTED;
+  if (s->dtype == PCTREE_F32 && (s->rank % 16 != 0 || s->rank > PCTREE_MAX_RANK_F32))
+    return PCTREE_ERR_UNSUPPORTED;
+  return PCTREE_OK;
+}
+
+pctree_status check_inputs(const pctree_inputs* in) {
+  if (!in || !in->base_logits || !in->emb || !in->proj_t || !in->depth_feat || !in->root_token ||
+      !in->prefix_len)
+    return PCTREE_ERR_INVALID_ARGUMENT;
+  if (!aligned(in->base_logits, 16) || !aligned(in->emb, 16) || !aligned(in->proj_t, 16) ||
+      !aligned(in->depth_feat, 16) || !aligned(in->root_token, 4) || !aligned(in->prefix_len, 4))
+    return PCTREE_ERR_INVALID_ARGUMENT;
+  return PCTREE_OK;
+}
+
+// Chain decode runs the tree builder with k = 1 and N = B + 1; its tree
+// outputs other than tokens and log-probabilities live in the workspace.
+struct ChainScratch {
+  size_t parent, depth, position, count, total;
+};
+
+ChainScratch chain_scratch(int R, int B) {
+  ChainScratch c;
+  const size_t row = align256((size_t)R * (B + 1) * sizeof(int32_t));
+  c.parent = 0;
+  c.depth = row;
+  c.position = 2 * row;
+  c.count = 3 * row;
+  c.total = 3 * row + align256((size_t)R * sizeof(int32_t));
+  return c;
+}
+
+size_t tree_bytes(const pctree_shape* s) {
+  Plan p{};
+  plan_shape(p, s->vocab, s->block, s->budget, s->topk, s->rank, s->requests, s->dtype);
+  return carve_workspace(p, nullptr);
+}
+
+size_t chain_bytes(const pctree_shape* s) {
+  Plan p{};
+  plan_shape(p, s->vocab, s->block, s->block + 1, 1, s->rank, s->requests, s->dtype);
+  return carve_workspace(p, nullptr) + chain_scratch(s->requests, s->block).total;
+}
+
+void bind_inputs(Plan& p, const pctree_inputs* in) {
+  p.L = in->base_logits;
+  p.E = in->emb;
+  p.Wt = in->proj_t;
+  p.h = in->depth_feat;
+  p.root = in->root_token;
+  p.prefix = in->prefix_len;
+}
+
+pctree_status enqueue(const Plan& p, void* stream) {
+  (void)hipGetLastError();  // start from a clean error state
+  const hipError_t e = launch_round(p, (hipStream_t)stream);
+  return e == hipSuccess ? PCTREE_OK : PCTREE_ERR_HIP;
+}
+
+}  // namespace
+
+void plan_shape(Plan& p, int V, int B, int N, int k, int r, int R, int dtype) {
+  p.V = V;
+  p.B = B;
+  p.N = N;
+  p.k = k;
+  p.kk = std::min(k, V);
+  p.r = r;
+  p.R = R;
+  p.dtype = dtype;
+  p.kmax = pow2ceil(p.kk);
+  p.nchunk = dtype ? r / 32 : r / 16;
+  p.ntiles = (V + kTile - 1) / kTile;
+  p.tiles_per_slice = std::max(4, (p.ntiles + kSlicesMax - 1) / kSlicesMax);
+  p.G = (p.ntiles + p.tiles_per_slice - 1) / p.tiles_per_slice;
+  p.maxpool = 1 + p.kk + (B - 1) * p.kk * p.kk;
+  p.rows_max = R * p.kk;
+}
+
+size_t carve_workspace(Plan& p, char* base) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> char* {
+    char* ptr = base ? base + off : nullptr;
+    off += align256(bytes);
+    return ptr;
+  };
+  const size_t R = p.R, kk = p.kk, es = p.dtype ? 2 : 4;
+  p.U = take(R * kk * p.r * es);
+  p.front_node = (int*)take(R * kk * sizeof(int));
+  p.front_tok = (int*)take(R * kk * sizeof(int));
+  p.front_score = (float*)take(R * kk * sizeof(float));
+  p.node_tok = (int*)take(R * p.maxpool * sizeof(int));
+  p.node_par = (int*)take(R * p.maxpool * sizeof(int));
+  p.node_depth = (int*)take(R * p.maxpool * sizeof(int));
+  p.node_score = (float*)take(R * p.maxpool * sizeof(float));
+  p.top_key = (uint64_t*)take(2 * R * p.N * sizeof(uint64_t));
+  p.top_node = (int*)take(2 * R * p.N * sizeof(int));
+  p.part_key = (uint64_t*)take((size_t)p.G * p.rows_max * p.kmax * sizeof(uint64_t));
+  p.part_ms = (float2*)take((size_t)p.G * p.rows_max * sizeof(float2));
+  p.req_bad = (int*)take(R * sizeof(int));
+  return off;
+}
+
+}  // namespace pctree
+
+using namespace pctree;
+
+extern "C" {
+
+size_t pctree_workspace_bytes(const pctree_shape* shape) {
+  if (check_shape(shape) != PCTREE_OK) return 0;
+  return std::max(tree_bytes(shape), chain_bytes(shape));
+}
+
+pctree_status pctree_build_tree(const pctree_shape* shape, const pctree_inputs* in,
+                                const pctree_tree* out, const pctree_trace* trace,
+                                void* workspace, size_t workspace_bytes, void* stream) {
+  try {
+    pctree_status st = check_shape(shape);
+    if (st != PCTREE_OK) return st;
+    if ((st = check_inputs(in)) != PCTREE_OK) return st;
+    if (!out || !out->token || !out->parent || !out->depth || !out->position || !out->logprob ||
+        !out->count)
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    if (!aligned(out->token, 4) || !aligned(out->parent, 4) || !aligned(out->depth, 4) ||
+        !aligned(out->position, 4) || !aligned(out->logprob, 4) || !aligned(out->count, 4) ||
+        !aligned(out->mask, 4))
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    if (trace && (!trace->token || !trace->parent_slot || !trace->score ||
+                  !aligned(trace->token, 4) || !aligned(trace->parent_slot, 4) ||
+                  !aligned(trace->score, 4)))
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    if (!workspace || !aligned(workspace, 256)) return PCTREE_ERR_WORKSPACE;
+
+    Plan p{};
+    plan_shape(p, shape->vocab, shape->block, shape->budget, shape->topk, shape->rank,
+               shape->requests, shape->dtype);
+    if (workspace_bytes < carve_workspace(p, nullptr)) return PCTREE_ERR_WORKSPACE;
+    carve_workspace(p, (char*)workspace);
+    bind_inputs(p, in);
+    p.o_token = out->token;
+    p.o_parent = out->parent;
+    p.o_depth = out->depth;
+    p.o_position = out->position;
+    p.o_logprob = out->logprob;
+    p.o_count = out->count;
+    p.o_mask = out->mask;
+    p.t_token = trace ? trace->token : nullptr;
+    p.t_pslot = trace ? trace->parent_slot : nullptr;
+    p.t_score = trace ? trace->score : nullptr;
+    return enqueue(p, stream);
+  } catch (...) {
+    return PCTREE_ERR_HIP;
+  }
+}
+
+pctree_status pctree_build_mask(const int32_t* parent, const int32_t* count, int32_t requests,
+                                int32_t budget, uint32_t* mask, void* stream) {
+  try {
+    if (!parent || !count || !mask || requests < 1 || budget < 1)
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    if (!aligned(parent, 4) || !aligned(count, 4) || !aligned(mask, 4))
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    if (budget > PCTREE_MAX_MASK_BUDGET || requests > 65535) return PCTREE_ERR_UNSUPPORTED;
+    (void)hipGetLastError();
+    const hipError_t e = launch_mask(parent, count, requests, budget, mask, (hipStream_t)stream);
+    return e == hipSuccess ? PCTREE_OK : PCTREE_ERR_HIP;
+  } catch (...) {
+    return PCTREE_ERR_HIP;
+  }
+}
+
+pctree_status pctree_chain_decode(const pctree_shape* shape, const pctree_inputs* in,
+                                  int32_t* chain_token, float* chain_logprob, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  try {
+    if (!shape) return PCTREE_ERR_INVALID_ARGUMENT;
+    pctree_shape cs = *shape;
+    cs.topk = 1;
+    cs.budget = std::max(1, std::min(shape->block, PCTREE_MAX_BLOCK) + 1);
+    pctree_status st = check_shape(&cs);
+    if (st != PCTREE_OK) return st;
+    if ((st = check_inputs(in)) != PCTREE_OK) return st;
+    if (!chain_token || !chain_logprob || !aligned(chain_token, 4) || !aligned(chain_logprob, 4))
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    if (!workspace || !aligned(workspace, 256)) return PCTREE_ERR_WORKSPACE;
+    if (workspace_bytes < chain_bytes(&cs)) return PCTREE_ERR_WORKSPACE;
+
+    Plan p{};
+    plan_shape(p, cs.vocab, cs.block, cs.budget, 1, cs.rank, cs.requests, cs.dtype);
+    const size_t tb = carve_workspace(p, (char*)workspace);
+    const ChainScratch c = chain_scratch(cs.requests, cs.block);
+    char* sb = (char*)workspace + tb;
+    bind_inputs(p, in);
+    p.o_token = chain_token;
+    p.o_logprob = chain_logprob;
+    p.o_parent = (int*)(sb + c.parent);
+    p.o_depth = (int*)(sb + c.depth);
+    p.o_position = (int*)(sb + c.position);
+    p.o_count = (int*)(sb + c.count);
+    p.o_mask = nullptr;
+    p.t_token = nullptr;
+    p.t_pslot = nullptr;
+    p.t_score = nullptr;
+    return enqueue(p, stream);
+  } catch (...) {
+    return PCTREE_ERR_HIP;
+  }
+}
+
+const char* pctree_status_string(pctree_status status) {
+  switch (status) {
+    case PCTREE_OK: return "PCTREE_OK";
+    case PCTREE_ERR_INVALID_ARGUMENT: return "PCTREE_ERR_INVALID_ARGUMENT";
+    case PCTREE_ERR_UNSUPPORTED: return "PCTREE_ERR_UNSUPPORTED";
+    case PCTREE_ERR_WORKSPACE: return "PCTREE_ERR_WORKSPACE";
+    case PCTREE_ERR_HIP: return "PCTREE_ERR_HIP";
+  }
+  return "PCTREE_ERR_UNKNOWN";
+}
+
+int32_t pctree_abi_version(void) { return PCTREE_ABI_VERSION; }
+
+}  // extern "C"

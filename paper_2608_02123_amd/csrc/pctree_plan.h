@@ -1,0 +1,84 @@
+// Internal launch plan shared by the C ABI (pctree_api.hip) and the kernels
+// (pctree_kernels.hip).  Not part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pctree {
+
+constexpr int kTile = 16;           // tokens per MFMA output tile (M of 16x16xK)
+constexpr int kSlicesMax = 512;     // V-slices of one head launch
+constexpr int kHeadThreads = 256;   // 4 waves
+constexpr int kSelectThreads = 1024;
+constexpr int kEmitThreads = 256;
+constexpr int kMaskThreads = 256;
+
+// Everything one round needs, passed by value to every kernel.
+struct Plan {
+  // problem size
+  int V, B, N, k, kk, r, R, dtype;  // kk = min(k, V); dtype 0 = f32, 1 = bf16
+  int kmax;                         // per-row candidate list length: pow2 >= kk
+  int nchunk;                       // 16-byte rank chunks per row: r/32 (bf16), r/16 (f32)
+  int G, tiles_per_slice, ntiles;   // head-stream V-slicing
+  int maxpool;                      // 1 + kk + (B-1) kk^2
+  int rows_max;                     // R * kk
+
+  // inputs
+  const void* L;
+  const void* E;
+  const void* Wt;
+  const float* h;
+  const int* root;
+  const int* prefix;
+
+  // outputs
+  int* o_token;
+  int* o_parent;
+  int* o_depth;
+  int* o_position;
+  int* o_count;
+  float* o_logprob;
+  uint32_t* o_mask;  // may be null
+  int* t_token;      // trace, may be null
+  int* t_pslot;
+  float* t_score;
+
+  // workspace
+  void* U;           // [R][kk][r] head activations of the current frontier (dtype)
+  int* front_node;   // [R][kk] pool id of each frontier slot
+  int* front_tok;    // [R][kk]
+  float* front_score;// [R][kk]
+  int* node_tok;     // [R][maxpool] candidate pool
+  int* node_par;     // [R][maxpool] pool id of the parent
+  int* node_depth;   // [R][maxpool]
+  float* node_score; // [R][maxpool]
+  uint64_t* top_key; // [2][R][N] running global top-N (sorted, descending)
+  int* top_node;     // [2][R][N]
+  uint64_t* part_key;// [G][rows_max][kmax] per-slice candidate lists
+  float2* part_ms;   // [G][rows_max] per-slice (row max, sum of exp)
+  int* req_bad;      // [R] root token outside [0, V)
+};
+
+// Workspace layout for a plan; offsets are 256-byte aligned.  With base ==
+// nullptr only the total is computed.
+size_t carve_workspace(Plan& p, char* base);
+
+// Fill the shape-derived fields of a plan (no pointers).
+void plan_shape(Plan& p, int V, int B, int N, int k, int r, int R, int dtype);
+
+// Enqueue one full round on `stream`.
+hipError_t launch_round(const Plan& p, hipStream_t stream);
+
+// Event bracketing of the dominant kernel (pctree_profile.hip): call
+// profile_mark() right before and right after each of its launches.
+bool profile_on();
+void profile_mark(hipStream_t stream);
+const char* dominant_kernel_name();
+
+// Enqueue the standalone ancestor-mask kernel.
+hipError_t launch_mask(const int* parent, const int* count, int R, int N, uint32_t* mask,
+                       hipStream_t stream);
+
+}  // namespace pctree

@@ -1,0 +1,81 @@
+// Optional hipEvent bracketing of the dominant kernel's launches (see
+// include/pctree_profile.h).  Off by default; costs one branch per launch.
+#include "pctree_profile.h"
+
+#include <mutex>
+#include <vector>
+
+#include "pctree_plan.h"
+
+namespace pctree {
+namespace {
+
+struct Recorder {
+  std::mutex mu;
+  bool on = false;
+  std::vector<hipEvent_t> pool;  // start/stop pairs, reused across enables
+  size_t used = 0;               // events handed out since enabling
+};
+
+Recorder& rec() {
+  static Recorder r;
+  return r;
+}
+
+hipEvent_t next_event() {
+  Recorder& r = rec();
+  if (r.used == r.pool.size()) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    r.pool.push_back(e);
+  }
+  return r.pool[r.used++];
+}
+
+}  // namespace
+
+bool profile_on() { return rec().on; }
+
+void profile_mark(hipStream_t stream) {
+  Recorder& r = rec();
+  std::lock_guard<std::mutex> g(r.mu);
+  if (!r.on) return;
+  hipEvent_t e = next_event();
+  if (e) hipEventRecord(e, stream);
+}
+
+}  // namespace pctree
+
+using namespace pctree;
+
+extern "C" {
+
+pctree_status pctree_profile_enable(int32_t enable) {
+  Recorder& r = rec();
+  std::lock_guard<std::mutex> g(r.mu);
+  r.on = enable != 0;
+  r.used = 0;
+  return PCTREE_OK;
+}
+
+pctree_status pctree_profile_read(double* total_ms, int64_t* launches, const char** kernel) {
+  if (!total_ms || !launches) return PCTREE_ERR_INVALID_ARGUMENT;
+  Recorder& r = rec();
+  std::lock_guard<std::mutex> g(r.mu);
+  double sum = 0.0;
+  const size_t pairs = r.used / 2;
+  for (size_t i = 0; i < pairs; ++i) {
+    float ms = 0.0f;
+    if (hipEventSynchronize(r.pool[2 * i + 1]) != hipSuccess ||
+        hipEventElapsedTime(&ms, r.pool[2 * i], r.pool[2 * i + 1]) != hipSuccess)
+      return PCTREE_ERR_HIP;
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = (int64_t)pairs;
+  if (kernel) *kernel = dominant_kernel_name();
+  r.used = 0;
+  return PCTREE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,274 @@
+"""Python binding of ``libpctree.so`` (the C ABI declared in include/pctree.h).
+
+Argument marshalling only: every step of a round runs in the library's HIP
+kernels.  torch supplies device memory and the current HIP stream.  If the
+library has not been built this module raises; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "PCTreeError",
+    "lib",
+    "Shape",
+    "workspace_bytes",
+    "build_tree",
+    "build_mask",
+    "chain_decode",
+    "TreeBuilder",
+    "status_string",
+    "F32",
+    "BF16",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpctree.so")
+
+OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
+F32, BF16 = 0, 1
+
+
+class PCTreeError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_string(status)}")
+        self.status = status
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("vocab", "block", "budget", "topk", "rank", "requests", "dtype", "mode")]
+
+
+class _Inputs(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("base_logits", "emb", "proj_t", "depth_feat", "root_token", "prefix_len")]
+
+
+class _Tree(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("token", "parent", "depth", "position", "logprob", "count", "mask")]
+
+
+class _Trace(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("token", "parent_slot", "score")]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; "
+                "g.build()'` (the HIP library is required; there is no CPU fallback)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, sz = ctypes.c_void_p, ctypes.c_size_t
+        L.pctree_workspace_bytes.argtypes = [ctypes.POINTER(Shape)]
+        L.pctree_workspace_bytes.restype = sz
+        L.pctree_build_tree.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(_Inputs),
+                                        ctypes.POINTER(_Tree), ctypes.POINTER(_Trace), vp, sz, vp]
+        L.pctree_build_tree.restype = ctypes.c_int
+        L.pctree_build_mask.argtypes = [vp, vp, ctypes.c_int32, ctypes.c_int32, vp, vp]
+        L.pctree_build_mask.restype = ctypes.c_int
+        L.pctree_chain_decode.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(_Inputs), vp, vp,
+                                          vp, sz, vp]
+        L.pctree_chain_decode.restype = ctypes.c_int
+        L.pctree_status_string.argtypes = [ctypes.c_int]
+        L.pctree_status_string.restype = ctypes.c_char_p
+        L.pctree_abi_version.argtypes = []
+        L.pctree_abi_version.restype = ctypes.c_int32
+        L.pctree_profile_enable.argtypes = [ctypes.c_int32]
+        L.pctree_profile_enable.restype = ctypes.c_int
+        L.pctree_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double),
+                                          ctypes.POINTER(ctypes.c_int64),
+                                          ctypes.POINTER(ctypes.c_char_p)]
+        L.pctree_profile_read.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().pctree_status_string(status).decode()
+
+
+def _check(status: int, what: str) -> None:
+    if status != OK:
+        raise PCTreeError(status, what)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}: float32 or bfloat16 expected")
+
+
+def make_shape(V, B, N, k, r, R, dtype, mode=0) -> Shape:
+    return Shape(V, B, N, k, r, R, dtype, mode)
+
+
+def workspace_bytes(V, B, N, k, r, R=1, dtype=BF16) -> int:
+    return int(lib().pctree_workspace_bytes(ctypes.byref(make_shape(V, B, N, k, r, R, dtype))))
+
+
+def _inputs(L, E, Wt, h, root, prefix_len):
+    for name, t in (("L", L), ("E", E), ("Wt", Wt), ("h", h), ("root", root),
+                    ("prefix_len", prefix_len)):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous device tensor")
+    if not (L.dtype == E.dtype == Wt.dtype):
+        raise TypeError("L, E and Wt must share one dtype")
+    if h.dtype != torch.float32 or root.dtype != torch.int32 or prefix_len.dtype != torch.int32:
+        raise TypeError("h must be float32; root and prefix_len int32")
+    return _Inputs(*(t.data_ptr() for t in (L, E, Wt, h, root, prefix_len)))
+
+
+class TreeBuilder:
+    """Pre-allocated outputs and workspace for repeated rounds of one shape.
+
+    ``run(L, E, Wt, h, root, prefix_len)`` enqueues one round on the current
+    stream and returns the output tensors (overwritten by the next call).
+    """
+
+    def __init__(self, V, B, N, k, r, R=1, dtype=BF16, device="cuda", mask=True, trace=False):
+        self.shape = make_shape(V, B, N, k, r, R, dtype)
+        nbytes = int(lib().pctree_workspace_bytes(ctypes.byref(self.shape)))
+        if nbytes == 0:
+            _check(lib().pctree_build_tree(ctypes.byref(self.shape), None, None, None, None, 0,
+                                           None), "shape")
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        i32 = dict(dtype=torch.int32, device=device)
+        self.out = {
+            "token": torch.empty(R, N, **i32),
+            "parent": torch.empty(R, N, **i32),
+            "depth": torch.empty(R, N, **i32),
+            "position": torch.empty(R, N, **i32),
+            "logprob": torch.empty(R, N, dtype=torch.float32, device=device),
+            "count": torch.empty(R, **i32),
+        }
+        if mask:
+            self.out["mask"] = torch.empty(R, N, (N + 31) // 32, **i32)
+        self._tree = _Tree(*(self.out[n].data_ptr() for n in
+                             ("token", "parent", "depth", "position", "logprob", "count")),
+                           self.out["mask"].data_ptr() if mask else None)
+        self._trace = None
+        if trace:
+            self.out["trace_token"] = torch.empty(R, B, k, **i32)
+            self.out["trace_parent_slot"] = torch.empty(R, B, k, **i32)
+            self.out["trace_score"] = torch.empty(R, B, k, dtype=torch.float32, device=device)
+            self._trace = _Trace(self.out["trace_token"].data_ptr(),
+                                 self.out["trace_parent_slot"].data_ptr(),
+                                 self.out["trace_score"].data_ptr())
+
+    def run(self, L, E, Wt, h, root, prefix_len, stream=None):
+        self.bind(L, E, Wt, h, root, prefix_len)
+        return self.launch(stream)
+
+    def bind(self, L, E, Wt, h, root, prefix_len):
+        """Check and remember the inputs once; ``launch()`` then only enqueues."""
+        self._inp = _inputs(L, E, Wt, h, root, prefix_len)
+        self._keep = (L, E, Wt, h, root, prefix_len)
+        self._args = (ctypes.byref(self.shape), ctypes.byref(self._inp), ctypes.byref(self._tree),
+                      ctypes.byref(self._trace) if self._trace is not None else None,
+                      ctypes.c_void_p(self.workspace.data_ptr()), self.workspace.numel())
+
+    def launch(self, stream=None):
+        st = lib().pctree_build_tree(*self._args, _stream(stream))
+        _check(st, "pctree_build_tree")
+        return self.out
+
+
+def build_tree(L, E, Wt, h, root, prefix_len, k, N, *, mask=True, trace=False, stream=None):
+    """One round for tensors ``L [R][B][V]``, ``E [V][r]``, ``Wt [V][r]``, ``h [R][B][r]``.
+
+    Returns a dict of freshly allocated output tensors (see include/pctree.h).
+    """
+    R, B, V = L.shape
+    r = E.shape[1]
+    b = TreeBuilder(V, B, N, k, r, R, _dtype_code(L), device=L.device, mask=mask, trace=trace)
+    return b.run(L, E, Wt, h, root, prefix_len, stream=stream)
+
+
+def profile_enable(on: bool = True) -> None:
+    """Bracket the dominant kernel's launches with hipEvents (include/pctree_profile.h)."""
+    _check(lib().pctree_profile_enable(1 if on else 0), "pctree_profile_enable")
+
+
+def profile_read():
+    """(total milliseconds, launches, kernel name) recorded since enabling; clears them."""
+    ms, n, name = ctypes.c_double(), ctypes.c_int64(), ctypes.c_char_p()
+    _check(lib().pctree_profile_read(ctypes.byref(ms), ctypes.byref(n), ctypes.byref(name)),
+           "pctree_profile_read")
+    return ms.value, n.value, name.value.decode()
+
+
+def build_mask(parent, count, stream=None):
+    """Ancestor mask ``[R][N][ceil(N/32)]`` (int32 view of uint32 words)."""
+    if parent.dtype != torch.int32 or count.dtype != torch.int32:
+        raise TypeError("parent and count must be int32")
+    if not (parent.is_cuda and count.is_cuda and parent.is_contiguous()):
+        raise ValueError("parent and count must be contiguous device tensors")
+    R, N = parent.shape
+    mask = torch.empty(R, N, (N + 31) // 32, dtype=torch.int32, device=parent.device)
+    st = lib().pctree_build_mask(_ptr(parent), _ptr(count), R, N, _ptr(mask), _stream(stream))
+    _check(st, "pctree_build_mask")
+    return mask
+
+
+def chain_decode(L, E, Wt, h, root, prefix_len=None, stream=None):
+    """The greedy chain of Eq. 1: returns (tokens [R][B+1], cumulative logprobs [R][B+1])."""
+    R, B, V = L.shape
+    r = E.shape[1]
+    if prefix_len is None:
+        prefix_len = torch.zeros(R, dtype=torch.int32, device=L.device)
+    shape = make_shape(V, B, 1, 1, r, R, _dtype_code(L))
+    nbytes = int(lib().pctree_workspace_bytes(ctypes.byref(shape)))
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=L.device)
+    toks = torch.empty(R, B + 1, dtype=torch.int32, device=L.device)
+    lps = torch.empty(R, B + 1, dtype=torch.float32, device=L.device)
+    inp = _inputs(L, E, Wt, h, root, prefix_len)
+    st = lib().pctree_chain_decode(ctypes.byref(shape), ctypes.byref(inp), _ptr(toks), _ptr(lps),
+                                   ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream))
+    _check(st, "pctree_chain_decode")
+    return toks, lps
+
+
+def device_inputs(inp: dict, device="cuda") -> dict:
+    """Upload one round's host inputs (the dict returned by ``synth.make_inputs``).
+
+    The head matrix is stored transposed, ``Wt [V][r]`` (each token's rank
+    vector contiguous, the same layout as ``E``); this packing is done once,
+    when the drafter's weights are loaded, not per round.
+    """
+    import numpy as np
+
+    dt = torch.bfloat16 if inp["workload"].dtype == "bf16" else torch.float32
+
+    def up(a, dtype):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(device=device).to(dtype)
+
+    return {
+        "L": up(inp["L"], dt),
+        "E": up(inp["E"], dt),
+        "Wt": up(inp["W"].T, dt),
+        "h": up(inp["h"], torch.float32),
+        "root": up(inp["root"], torch.int32),
+        "prefix_len": up(inp["prefix_len"], torch.int32),
+    }

@@ -70,13 +70,15 @@ CONFIGS = {
 def round_to_bf16(x: np.ndarray) -> np.ndarray:
     """Round float64 values once, to nearest-even, onto the bfloat16 grid.
 
+    Works on the float64 bit pattern: bfloat16 keeps 7 of the 52 stored
+    mantissa bits, so the low 45 bits are rounded away (ties to even).
     Returns float32 values that are exactly representable in bfloat16.
-    (Finite, normal-range inputs only; the generator never produces others.)
+    (Finite inputs within the float32 normal range, or zero.)
     """
-    x = np.asarray(x, dtype=np.float64)
-    m, e = np.frexp(x)  # x = m * 2**e with 0.5 <= |m| < 1
-    q = np.rint(m * 256.0)  # 8 significant bits, ties to even
-    return np.ldexp(q / 256.0, e).astype(np.float32)
+    b = np.ascontiguousarray(x, dtype=np.float64).view(np.uint64)
+    lsb = (b >> np.uint64(45)) & np.uint64(1)
+    b = (b + (np.uint64((1 << 44) - 1) + lsb)) & ~np.uint64((1 << 45) - 1)
+    return b.view(np.float64).astype(np.float32)
 
 
 def bf16_bits(x32: np.ndarray) -> np.ndarray:

@@ -1,0 +1,151 @@
+"""C ABI checks that need no GPU: the library loads, exports every function that
+include/pctree.h declares, and rejects bad arguments on the host before any
+device work (so every error status is reachable without a device)."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_02123_amd import pctree as P
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "pctree.h")
+A = 0x100000  # fake, suitably aligned device addresses (validation never dereferences)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(pctree_\w+)\s*\(", text, re.M)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert {"pctree_build_tree", "pctree_build_mask", "pctree_chain_decode",
+            "pctree_workspace_bytes", "pctree_status_string", "pctree_abi_version"} <= set(names)
+    lib = ctypes.CDLL(P.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert P.lib().pctree_abi_version() == 1
+
+
+def test_status_strings():
+    for code, name in enumerate(["PCTREE_OK", "PCTREE_ERR_INVALID_ARGUMENT",
+                                 "PCTREE_ERR_UNSUPPORTED", "PCTREE_ERR_WORKSPACE",
+                                 "PCTREE_ERR_HIP"]):
+        assert P.status_string(code) == name
+    assert P.status_string(99) == "PCTREE_ERR_UNKNOWN"
+
+
+def shape(**kw):
+    base = dict(vocab=151936, block=16, budget=64, topk=8, rank=256, requests=1, dtype=P.BF16,
+                mode=0)
+    base.update(kw)
+    return P.Shape(*(base[n] for n, _ in P.Shape._fields_))
+
+
+def inputs(**kw):
+    base = {n: A + 0x1000 * i for i, (n, _) in enumerate(P._Inputs._fields_)}
+    base.update(kw)
+    return P._Inputs(*(base[n] for n, _ in P._Inputs._fields_))
+
+
+def tree(**kw):
+    base = {n: A + 0x100000 + 0x1000 * i for i, (n, _) in enumerate(P._Tree._fields_)}
+    base.update(kw)
+    return P._Tree(*(base[n] for n, _ in P._Tree._fields_))
+
+
+def build(s=None, i=None, t=None, tr=None, ws=A * 16, nbytes=None):
+    s = s if s is not None else shape()
+    if nbytes is None:
+        nbytes = P.lib().pctree_workspace_bytes(ctypes.byref(s)) if s else 0
+    return P.lib().pctree_build_tree(
+        ctypes.byref(s) if s is not None else None,
+        ctypes.byref(i) if i is not None else None,
+        ctypes.byref(t) if t is not None else None,
+        ctypes.byref(tr) if tr is not None else None,
+        ctypes.c_void_p(ws) if ws else None, nbytes, None)
+
+
+@pytest.mark.parametrize("field", ["vocab", "block", "budget", "topk", "rank", "requests"])
+def test_nonpositive_sizes_are_invalid(field):
+    assert build(shape(**{field: 0}), inputs(), tree()) == P.ERR_INVALID_ARGUMENT
+    assert build(shape(**{field: -3}), inputs(), tree()) == P.ERR_INVALID_ARGUMENT
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=7), P.ERR_INVALID_ARGUMENT),
+    (dict(mode=1), P.ERR_UNSUPPORTED),
+    (dict(vocab=(1 << 20) + 1), P.ERR_UNSUPPORTED),
+    (dict(block=64), P.ERR_UNSUPPORTED),
+    (dict(topk=17), P.ERR_UNSUPPORTED),
+    (dict(budget=257), P.ERR_UNSUPPORTED),
+    (dict(requests=257), P.ERR_UNSUPPORTED),
+    (dict(rank=48), P.ERR_UNSUPPORTED),
+    (dict(rank=544), P.ERR_UNSUPPORTED),
+    (dict(dtype=P.F32, rank=40), P.ERR_UNSUPPORTED),
+    (dict(dtype=P.F32, rank=144), P.ERR_UNSUPPORTED),
+])
+def test_shape_limits(kw, code):
+    assert build(shape(**kw), inputs(), tree()) == code
+    assert P.lib().pctree_workspace_bytes(ctypes.byref(shape(**kw))) == 0
+
+
+def test_null_and_misaligned_pointers():
+    assert P.lib().pctree_build_tree(None, None, None, None, None, 0, None) == \
+        P.ERR_INVALID_ARGUMENT
+    assert build(i=None, t=tree()) == P.ERR_INVALID_ARGUMENT
+    for n, _ in P._Inputs._fields_:
+        assert build(i=inputs(**{n: 0}), t=tree()) == P.ERR_INVALID_ARGUMENT, n
+    assert build(i=inputs(proj_t=A + 8), t=tree()) == P.ERR_INVALID_ARGUMENT
+    assert build(i=inputs(root_token=A + 2), t=tree()) == P.ERR_INVALID_ARGUMENT
+    assert build(i=inputs(), t=None) == P.ERR_INVALID_ARGUMENT
+    for n, _ in P._Tree._fields_:
+        if n != "mask":
+            assert build(i=inputs(), t=tree(**{n: 0})) == P.ERR_INVALID_ARGUMENT, n
+    assert build(i=inputs(), t=tree(logprob=A + 2)) == P.ERR_INVALID_ARGUMENT
+    bad_trace = P._Trace(A, 0, A)
+    assert build(i=inputs(), t=tree(), tr=bad_trace) == P.ERR_INVALID_ARGUMENT
+
+
+def test_workspace_errors():
+    s = shape()
+    need = P.lib().pctree_workspace_bytes(ctypes.byref(s))
+    assert need > 0
+    assert build(s, inputs(), tree(), ws=0) == P.ERR_WORKSPACE
+    assert build(s, inputs(), tree(), ws=A * 16 + 128) == P.ERR_WORKSPACE
+    assert build(s, inputs(), tree(), nbytes=need - 1) == P.ERR_WORKSPACE
+
+
+def test_workspace_size_grows_with_the_problem():
+    ws = lambda **kw: P.lib().pctree_workspace_bytes(ctypes.byref(shape(**kw)))  # noqa: E731
+    assert ws(budget=128) >= ws(budget=64)
+    assert ws(topk=16) > ws(topk=8)
+    assert ws(requests=8) > ws(requests=1)
+    assert ws(block=32) > ws(block=16)
+    assert ws() % 256 == 0
+
+
+def test_build_mask_validation():
+    f = P.lib().pctree_build_mask
+    assert f(None, A, 1, 8, A, None) == P.ERR_INVALID_ARGUMENT
+    assert f(A, A, 0, 8, A, None) == P.ERR_INVALID_ARGUMENT
+    assert f(A, A, 1, 0, A, None) == P.ERR_INVALID_ARGUMENT
+    assert f(A + 1, A, 1, 8, A, None) == P.ERR_INVALID_ARGUMENT
+    assert f(A, A, 1, 1025, A, None) == P.ERR_UNSUPPORTED
+
+
+def test_chain_decode_validation():
+    f = P.lib().pctree_chain_decode
+    s = shape(topk=0, budget=0)  # ignored by the chain
+    vp = ctypes.c_void_p
+    assert f(ctypes.byref(shape(mode=2)), ctypes.byref(inputs()), vp(A), vp(A), vp(A * 16),
+             1 << 30, None) == P.ERR_UNSUPPORTED
+    assert f(ctypes.byref(s), ctypes.byref(inputs()), None, vp(A), vp(A * 16), 1 << 30,
+             None) == P.ERR_INVALID_ARGUMENT
+    assert f(ctypes.byref(s), ctypes.byref(inputs()), vp(A), vp(A), vp(A * 16), 64,
+             None) == P.ERR_WORKSPACE
+    assert f(ctypes.byref(s), None, vp(A), vp(A), vp(A * 16), 1 << 30,
+             None) == P.ERR_INVALID_ARGUMENT
