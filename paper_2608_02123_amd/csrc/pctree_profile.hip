@@ -41,7 +41,7 @@ void profile_mark(hipStream_t stream) {
   std::lock_guard<std::mutex> g(r.mu);
   if (!r.on) return;
   hipEvent_t e = next_event();
-  if (e) hipEventRecord(e, stream);
+  if (e) (void)hipEventRecord(e, stream);
 }
 
 }  // namespace pctree
