@@ -24,7 +24,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
 METRIC = "tree-build rounds/sec + µs/round (V=151936,B=16,N=64); % peak HBM GB/s"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "head_kernel_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "round_kernel_traffic.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2608_02123_amd", "csrc", "pctree_kernels.hip")
 
 
@@ -50,7 +50,7 @@ def kernel_hash():
 
 
 def measured_traffic():
-    """HBM bytes per head launch from rocprofv3 counters, if they were taken on
+    """HBM bytes per dominant-kernel launch from rocprofv3 counters, if taken on
     the current kernel source; else None."""
     try:
         with open(TRAFFIC_FILE) as f:
@@ -96,6 +96,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cold-steps", type=int, default=50)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run a 256 MiB device copy, the reference for HBM counters")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -109,6 +111,13 @@ def main():
     from paper_2608_02123_amd.synth import CONFIGS, make_inputs
 
     w = CONFIGS[args.workload]
+    if args.calibrate_copy:
+        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)  # reads 256 MiB, writes 256 MiB
+        torch.cuda.synchronize()
+        log("[bench] calibration copy done (3 x 256 MiB)")
     log(f"[bench] generating {w.name}")
     inp = make_inputs(w)
     torch.cuda.set_device(0)
@@ -145,7 +154,8 @@ def main():
     P.profile_enable(False)
     k_avg_s = kms / 1000.0 / max(launches, 1)
     bytes_round = algorithmic_bytes(w)
-    per_launch = bytes_round / w.B  # one head launch = one depth
+    # the persistent round kernel runs all B stages; a head launch runs one
+    per_launch = bytes_round if kname == "round_kernel" else bytes_round / w.B
     achieved = per_launch / k_avg_s / 1e9
 
     # cold-MALL rounds: a 512 MiB write between rounds evicts W from the

@@ -1,26 +1,37 @@
 // HIP kernels of the PCTree per-round tree builder for gfx950 (CDNA4).
 //
-// One round (Alg. 1) is enqueued as
-//   prologue                       root node, frontier {x_t}, head input of x_t
-//   for d in 0..B-1:
-//     head_stream   (G x CB WGs)   Z = 1 L_d^T + U W for the frontier rows on
-//                                  bf16/f32 MFMA, fused with an online row
-//                                  logsumexp and per-row top-k; the V-wide
-//                                  child logits never leave the chip (Eq. 2/3)
-//     select        (R WGs)        merge the V-slices, score children (Eq. 4),
-//                                  pick the next frontier (top-k of the layer)
-//                                  and update the running global top-N
-//   emit            (R WGs)        canonical emission + optional ancestor mask
+// A round (Alg. 1) runs B sequential Markov stages.  Stage d batches the
+// frontier parents (Eq. 3): Z = 1 L_d^T + U W with U = SiLU(E[parents] + h_d),
+// normalises every row (Eq. 2), keeps each parent's top-k children with path
+// scores (Eq. 4) and prunes the layer to k frontier nodes (Sec. 4.1); after B
+// stages the global top-N is emitted (Sec. 4.2, App. A).
+//
+// Every stage streams the whole head matrix W (V x r) once.  The V axis is cut
+// into slices; a workgroup streams its slice through bf16/f32 MFMA with the
+// parents as the 16 MFMA columns, folds each row into an online logsumexp and
+// a per-lane top-k list, and publishes one (max, sum, top-k) partial per row:
+// the V-wide child logits never leave the chip.  The partials of all slices
+// are then merged and the stage's selection runs.
+//
+// Two launch forms:
+//  * narrow (R * k' <= 16 frontier rows, one MFMA column block): ONE persistent
+//    cooperative kernel per round.  After each stage the last workgroup to
+//    arrive merges the slices, selects, writes the next frontier's head input
+//    and releases the others; the last stage's selector also emits the tree.
+//  * wide (more rows): per stage a head launch over (slice, column block) and a
+//    per-request select launch; then an emit launch.
 //
 // Ordering keys are unique 64-bit integers, so every selection is exact and
 // deterministic:
-//   child key  = ord(z)     << 32 | ~token                       (z desc, token asc)
-//   node key   = ord(score) << 32 | (63-depth) << 26 | (2^20-1-token) << 6 | (63-slot)
-//                                        (score desc, depth asc, token asc, slot asc)
-// where ord() maps a float to an unsigned integer of the same order (-0 -> +0).
+//   child key = ord(z)     << 32 | ~token                          (z desc, token asc)
+//   node key  = ord(score) << 32 | (63-depth) << 26 | (2^20-1-token) << 6 | (63-slot)
+//                                         (score desc, depth asc, token asc, slot asc)
+// where ord() maps a float onto an unsigned integer of the same order (-0 -> +0).
 #include "pctree_plan.h"
 
 #include <math.h>
+
+#include <algorithm>
 
 #define PCTREE_EMIT_MAX_N 256
 #define PCTREE_MASK_MAX_N 1024
@@ -34,6 +45,11 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegBig = -3.0e38f;  // "no value yet" for running maxima
+constexpr int kHeadsPerLane = kSlicesMax / 64;
+
+__device__ __forceinline__ void __atomic_thread_fence_agent_acquire() {
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
 
 __device__ __forceinline__ uint32_t f32_ord(float f) {
   uint32_t b = __float_as_uint(f);
@@ -80,18 +96,74 @@ __device__ __forceinline__ float load_elem(const void* base, size_t i) {
   return ((const float*)base)[i];
 }
 
-// Write the head input of one frontier row: U[row][0..r) = act(E[tok], h_d).
-__device__ void write_activation(const Plan& p, int row, int tok, const float* hd, int j0,
-                                 int stride) {
+// One head-input element of row `row` (request-major rows of kk slots):
+// u = act(E[tok][j], h[req][d][j]) stored at the head's precision.
+__device__ __forceinline__ void put_activation(const Plan& p, size_t row, int tok, int j,
+                                               float hj) {
+  const size_t o = row * p.r + j;
   if (p.dtype) {
-    uint16_t* u = (uint16_t*)p.U + (size_t)row * p.r;
-    const uint16_t* e = (const uint16_t*)p.E + (size_t)tok * p.r;
-    for (int j = j0; j < p.r; j += stride)
-      u[j] = bf16_rne(silu_f32(__uint_as_float((uint32_t)e[j] << 16), hd[j]));
+    const float ej =
+        __uint_as_float((uint32_t)((const uint16_t*)p.E)[(size_t)tok * p.r + j] << 16);
+    ((uint16_t*)p.U)[o] = bf16_rne(silu_f32(ej, hj));
   } else {
-    float* u = (float*)p.U + (size_t)row * p.r;
-    const float* e = (const float*)p.E + (size_t)tok * p.r;
-    for (int j = j0; j < p.r; j += stride) u[j] = silu_f32(e[j], hd[j]);
+    ((float*)p.U)[o] = silu_f32(((const float*)p.E)[(size_t)tok * p.r + j], hj);
+  }
+}
+
+// Selection state of a round: the frontier (slot-indexed, kk per request) and
+// the running global top-N (sorted keys and pool ids, N per request).  It
+// lives in the workspace for the multi-launch form and in the selector
+// workgroup's LDS for the persistent form.
+struct State {
+  int* front_node;
+  int* front_tok;
+  float* front_score;
+  uint64_t* top_key;
+  int* top_node;
+};
+
+__device__ __forceinline__ State global_state(const Plan& p) {
+  return State{p.front_node, p.front_tok, p.front_score, p.top_key, p.top_node};
+}
+
+// Head inputs of the frontier used at stage `d` for requests [req0, req0+nreq).
+// Each thread issues the loads of four elements before computing any of them.
+__device__ void write_activations(const Plan& p, const State& st, int d, int req0, int nreq) {
+  constexpr int kBatch = 4;
+  const int per_req = p.kk * p.r;
+  const int n = nreq * per_req;
+  for (int base = 0; base < n; base += kBatch * blockDim.x) {
+    size_t erow[kBatch], urow[kBatch], hrow[kBatch];
+    uint32_t ev[kBatch];
+    float hv[kBatch];
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) {
+      const int e = min(base + q * (int)blockDim.x + (int)threadIdx.x, n - 1);
+      const int rq = e / per_req;
+      const int rem = e - rq * per_req;
+      const int slot = rem / p.r;
+      const int j = rem - slot * p.r;
+      const int req = req0 + rq;
+      erow[q] = (size_t)st.front_tok[req * p.kk + slot] * p.r + j;
+      urow[q] = ((size_t)req * p.kk + slot) * p.r + j;
+      hrow[q] = ((size_t)req * p.B + d) * p.r + j;
+    }
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) {
+      ev[q] = p.dtype ? (uint32_t)((const uint16_t*)p.E)[erow[q]] << 16
+                      : ((const uint32_t*)p.E)[erow[q]];
+      hv[q] = p.h[hrow[q]];
+    }
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) {
+      if (base + q * (int)blockDim.x + (int)threadIdx.x < n) {
+        const float u = silu_f32(__uint_as_float(ev[q]), hv[q]);
+        if (p.dtype)
+          ((uint16_t*)p.U)[urow[q]] = bf16_rne(u);
+        else
+          ((float*)p.U)[urow[q]] = u;
+      }
+    }
   }
 }
 
@@ -141,6 +213,66 @@ __device__ __forceinline__ void list_merge_xor(uint64_t (&l)[K], int mask) {
   list_merge(l, o);
 }
 
+// Wave-wide reductions on DPP lane permutations (VALU latency, not the LDS
+// path of a shuffle): within each 16-lane row by quad permutes and mirrors,
+// then across rows by broadcasts of lanes 15 and 31; lane 63 ends with the
+// result, which is read back into a uniform value.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROWS, 0xF, false);
+}
+
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+  return ((uint64_t)dpp<CTRL, ROWS>((uint32_t)(v >> 32)) << 32) | dpp<CTRL, ROWS>((uint32_t)v);
+}
+
+__device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
+  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Keys are >= 0, so 0 (what DPP yields for lanes outside the row mask) is
+// the identity of the maximum.
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+  v = max_u64(v, dpp64<0xB1, 0xF>(v));   // quad_perm [1,0,3,2]
+  v = max_u64(v, dpp64<0x4E, 0xF>(v));   // quad_perm [2,3,0,1]
+  v = max_u64(v, dpp64<0x141, 0xF>(v));  // row_half_mirror
+  v = max_u64(v, dpp64<0x140, 0xF>(v));  // row_mirror
+  v = max_u64(v, dpp64<0x142, 0xA>(v));  // row_bcast15 into rows 1, 3
+  v = max_u64(v, dpp64<0x143, 0xC>(v));  // row_bcast31 into rows 2, 3
+  return readlane_u64(v, 63);
+}
+
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dppf(float v, float identity) {
+  return __uint_as_float((uint32_t)__builtin_amdgcn_update_dpp(
+      (int)__float_as_uint(identity), (int)__float_as_uint(v), CTRL, ROWS, 0xF, false));
+}
+
+__device__ __forceinline__ float wave_max_f32(float v) {
+  v = fmaxf(v, dppf<0xB1, 0xF>(v, kNegBig));
+  v = fmaxf(v, dppf<0x4E, 0xF>(v, kNegBig));
+  v = fmaxf(v, dppf<0x141, 0xF>(v, kNegBig));
+  v = fmaxf(v, dppf<0x140, 0xF>(v, kNegBig));
+  v = fmaxf(v, dppf<0x142, 0xA>(v, kNegBig));
+  v = fmaxf(v, dppf<0x143, 0xC>(v, kNegBig));
+  return __uint_as_float(__builtin_amdgcn_readlane((int)__float_as_uint(v), 63));
+}
+
+__device__ __forceinline__ float wave_sum_f32(float v) {
+  v += dppf<0xB1, 0xF>(v, 0.0f);
+  v += dppf<0x4E, 0xF>(v, 0.0f);
+  v += dppf<0x141, 0xF>(v, 0.0f);
+  v += dppf<0x140, 0xF>(v, 0.0f);
+  v += dppf<0x142, 0xA>(v, 0.0f);
+  v += dppf<0x143, 0xC>(v, 0.0f);
+  return __uint_as_float(__builtin_amdgcn_readlane((int)__float_as_uint(v), 63));
+}
+
 // (m, s) pairs describe sum_i exp(z_i) = exp(m) * s; combine two of them.
 __device__ __forceinline__ void lse_combine(float& m, float& s, float om, float os) {
   const float nm = fmaxf(m, om);
@@ -184,8 +316,13 @@ __global__ __launch_bounds__(kEmitThreads) void prologue_kernel(Plan p) {
   int root = p.root[req];
   const bool bad = root < 0 || root >= p.V;
   if (bad) root = 0;
+  if (req == 0) {
+    for (int i = tid; i < p.B + 1; i += blockDim.x) p.sync[i] = 0;
+    for (int g = tid; g < p.G; g += blockDim.x) p.flags[(size_t)g * kFlagStride] = 0;
+  }
   if (tid == 0) {
     p.req_bad[req] = bad ? 1 : 0;
+    p.o_count[req] = -1;  // stays -1 if the round is aborted before emission
     const size_t nb = (size_t)req * p.maxpool;
     p.node_tok[nb] = root;
     p.node_par[nb] = -1;
@@ -207,25 +344,50 @@ __global__ __launch_bounds__(kEmitThreads) void prologue_kernel(Plan p) {
       p.t_score[o] = first ? 0.0f : -INFINITY;
     }
   }
-  write_activation(p, req * p.kk, root, p.h + (size_t)req * p.B * p.r, tid, blockDim.x);
+  for (int j = tid; j < p.r; j += blockDim.x)
+    put_activation(p, (size_t)req * p.kk, root, j, p.h[(size_t)req * p.B * p.r + j]);
 }
 
 // ---------------------------------------------------------------------------
-// head stream: one WG per (V-slice, block of 16 frontier rows)
+// head stream over one V-slice for one block of 16 frontier rows
 // ---------------------------------------------------------------------------
 // MFMA 16x16xK with tokens as M and frontier rows as N: lane l feeds A row
 // (token) l%16 and B column (row) l%16 with rank chunk group l/16, and
 // receives C[token 4*(l/16)+i][row l%16], i = 0..3.
-template <int DT, int NCMAX, int KMAX>
-__global__ __launch_bounds__(kHeadThreads) void head_kernel(Plan p, int d, int P) {
-  constexpr int KC = DT ? 32 : 16;  // rank elements per 16-byte chunk quad
+template <int KMAX, int WAVES>
+struct HeadShared {
+  uint64_t wl[WAVES][kTile][KMAX];
+  float2 wms[WAVES][kTile];
+};
+
+template <int NCMAX>
+struct Tile {
+  u32x4 a[NCMAX];
+  uint32_t l[4];  // raw bits of L_d (bf16 in the low half, or f32)
+};
+
+template <int DT>
+__device__ __forceinline__ uint32_t load_raw(const void* base, size_t i) {
+  if (DT) return ((const uint16_t*)base)[i];
+  return ((const uint32_t*)base)[i];
+}
+
+template <int DT>
+__device__ __forceinline__ float raw_to_f32(uint32_t r) {
+  return __uint_as_float(DT ? r << 16 : r);
+}
+
+template <int DT, int NCMAX, int KMAX, int WAVES>
+__device__ __forceinline__ void head_slice(const Plan& p, int d, int P, int cb, int slice,
+                                           HeadShared<KMAX, WAVES>& sh) {
+  constexpr int KC = DT ? 32 : 16;  // rank elements per chunk (16 bytes per lane group)
   constexpr int ESZ = DT ? 2 : 4;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int col = lane & 15;
   const int grp = lane >> 4;
   const int rows = p.R * P;
-  const int row = blockIdx.y * kTile + col;
+  const int row = cb * kTile + col;
   const bool row_ok = row < rows;
   const int req = row_ok ? row / P : 0;
   const int slot = row_ok ? row - req * P : 0;
@@ -243,37 +405,39 @@ __global__ __launch_bounds__(kHeadThreads) void head_kernel(Plan p, int d, int P
     }
   }
   const size_t lrow = ((size_t)req * p.B + d) * p.V;
+  const char* wbase = (const char*)p.Wt + ((size_t)col * p.r + grp * (KC / 4)) * ESZ;
 
   float m = kNegBig, s = 0.0f;
   uint64_t list[KMAX];
 #pragma unroll
   for (int i = 0; i < KMAX; ++i) list[i] = 0;
 
-  const int t0 = blockIdx.x * p.tiles_per_slice;
-  const int t1 = min(t0 + p.tiles_per_slice, p.ntiles);
-  for (int t = t0 + wave; t < t1; t += kHeadThreads / 64) {
-    const int tokA = t * kTile + col;
-    const char* wrow = (const char*)p.Wt + ((size_t)tokA * p.r + grp * (KC / 4)) * ESZ;
-    u32x4 afrag[NCMAX];
-#pragma unroll
-    for (int c = 0; c < NCMAX; ++c) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (c < nc && tokA < p.V) v = *(const u32x4*)(wrow + (size_t)c * KC * ESZ);
-      afrag[c] = v;
-    }
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  // No branch in the load or MFMA path (a branch makes the compiler wait for
+  // every load in flight): token indices are clamped into the vocabulary, and
+  // chunks past the rank re-read the last chunk in bounds and meet zero B
+  // fragments.  Rows of tokens >= V are discarded in the epilogue.
+  auto load = [&](Tile<NCMAX>& T, int t) {
+    const int tokA = min(t * kTile + col, p.V - 1);
+    const char* wrow = wbase + ((size_t)tokA - col) * p.r * ESZ;
 #pragma unroll
     for (int c = 0; c < NCMAX; ++c)
-      if (c < nc) acc = mfma_chunk<DT>(afrag[c], bfrag[c], acc);
+      T.a[c] = *(const u32x4*)(wrow + (size_t)min(c, nc - 1) * KC * ESZ);
+    const int tb = t * kTile + grp * 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) T.l[i] = load_raw<DT>(p.L, lrow + min(tb + i, p.V - 1));
+  };
 
+  auto process = [&](const Tile<NCMAX>& T, int t) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NCMAX; ++c) acc = mfma_chunk<DT>(T.a[c], bfrag[c], acc);
     if (row_ok) {
       const int tb = t * kTile + grp * 4;
       float z[4];
       float tmax = kNegBig;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int tok = tb + i;
-        z[i] = tok < p.V ? acc[i] + load_elem<DT>(p.L, lrow + tok) : kNegBig;
+        z[i] = tb + i < p.V ? acc[i] + raw_to_f32<DT>(T.l[i]) : kNegBig;
         tmax = fmaxf(tmax, z[i]);
       }
       const float nm = fmaxf(m, tmax);
@@ -291,6 +455,42 @@ __global__ __launch_bounds__(kHeadThreads) void head_kernel(Plan p, int d, int P
         }
       }
     }
+  };
+
+  // software pipeline: the next tiles' loads are in flight while this one
+  // computes (three tiles in registers up to rank 256, else two).
+  // Prefetches are unconditional (clamped to the slice's last tile, surplus
+  // ones are never processed) so the compiler's waits stay partial.
+  const int t1 = min((slice + 1) * p.tiles_per_slice, p.ntiles);
+  int t = slice * p.tiles_per_slice + wave;
+  Tile<NCMAX> TA, TB;
+  load(TA, min(t, t1 - 1));
+  if constexpr (NCMAX <= 8) {
+    Tile<NCMAX> TC;
+    load(TB, min(t + WAVES, t1 - 1));
+    while (t < t1) {
+      load(TC, min(t + 2 * WAVES, t1 - 1));
+      process(TA, t);
+      t += WAVES;
+      if (t >= t1) break;
+      load(TA, min(t + 2 * WAVES, t1 - 1));
+      process(TB, t);
+      t += WAVES;
+      if (t >= t1) break;
+      load(TB, min(t + 2 * WAVES, t1 - 1));
+      process(TC, t);
+      t += WAVES;
+    }
+  } else {
+    while (t < t1) {
+      load(TB, min(t + WAVES, t1 - 1));
+      process(TA, t);
+      t += WAVES;
+      if (t >= t1) break;
+      load(TA, min(t + WAVES, t1 - 1));
+      process(TB, t);
+      t += WAVES;
+    }
   }
 
   // rows live in lanes col, col+16, col+32, col+48 of every wave
@@ -298,202 +498,245 @@ __global__ __launch_bounds__(kHeadThreads) void head_kernel(Plan p, int d, int P
   lse_combine_xor(m, s, 16);
   list_merge_xor(list, 32);
   lse_combine_xor(m, s, 32);
-
-  __shared__ uint64_t sh_list[kHeadThreads / 64][kTile][KMAX];
-  __shared__ float2 sh_ms[kHeadThreads / 64][kTile];
   if (grp == 0) {
 #pragma unroll
-    for (int i = 0; i < KMAX; ++i) sh_list[wave][col][i] = list[i];
-    sh_ms[wave][col] = make_float2(m, s);
+    for (int i = 0; i < KMAX; ++i) sh.wl[wave][col][i] = list[i];
+    sh.wms[wave][col] = make_float2(m, s);
   }
   __syncthreads();
   if (wave == 0) {
 #pragma unroll
-    for (int i = 0; i < KMAX; ++i) list[i] = sh_list[grp][col][i];
-    m = sh_ms[grp][col].x;
-    s = sh_ms[grp][col].y;
+    for (int i = 0; i < KMAX; ++i) list[i] = sh.wl[grp][col][i];
+    m = sh.wms[grp][col].x;
+    s = sh.wms[grp][col].y;
+#pragma unroll
+    for (int w = grp + 4; w < WAVES; w += 4) {
+      uint64_t o[KMAX];
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) o[i] = sh.wl[w][col][i];
+      list_merge(list, o);
+      lse_combine(m, s, sh.wms[w][col].x, sh.wms[w][col].y);
+    }
     list_merge_xor(list, 16);
     lse_combine_xor(m, s, 16);
     list_merge_xor(list, 32);
     lse_combine_xor(m, s, 32);
     if (grp == 0 && row_ok) {
-      const size_t o = (size_t)blockIdx.x * p.rows_max + row;
+      const size_t o = (size_t)row * kSlicesMax + slice;
       uint64_t* dst = p.part_key + o * KMAX;
 #pragma unroll
       for (int i = 0; i < KMAX; ++i) dst[i] = list[i];
+      p.part_head[o] = list[0];
       p.part_ms[o] = make_float2(m, s);
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// select: one WG per request after every head launch
+// stage selection on merged rows (shared by both launch forms)
 // ---------------------------------------------------------------------------
-template <int KMAX>
-__global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, int P) {
-  constexpr int NW = kSelectThreads / 64;
-  const int req = blockIdx.x;
+// Number of keys[0..n) greater than `key`; the loads of eight entries are
+// issued before any comparison (a dependent LDS read per entry would cost its
+// full latency n times).
+__device__ __forceinline__ int count_greater(const uint64_t* keys, int n, uint64_t key) {
+  int cnt = 0;
+  int c = 0;
+  for (; c + 8 <= n; c += 8) {
+    uint64_t v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = keys[c + i];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cnt += v[i] > key;
+  }
+  for (; c < n; ++c) cnt += keys[c] > key;
+  return cnt;
+}
+
+struct SelShared {
+  uint64_t rowkeys[kNarrowRows][16];  // top-k' children (child keys) of each row
+  float lse[kNarrowRows];
+  int win[kRoundWaves][16];           // slices holding a row's top-k' (per-wave scratch)
+  __attribute__((aligned(16))) uint64_t ckey[256];  // node keys of the stage's candidates
+  int rank[256];
+  __attribute__((aligned(16))) uint64_t tkey[PCTREE_EMIT_MAX_N];  // a request's top-N keys
+};
+
+// Candidates of the P rows of each request in [req0, req0 + nreq), whose
+// top-k' children and lse are in sh.rowkeys / sh.lse (request-major, row 0 =
+// request req0's slot 0): score them (Eq. 4), put them into the pool, pick the
+// next frontier (the k' best of each request's layer, Sec. 4.1), merge them
+// into the running global top-N (Sec. 4.2) and write the next head input.
+// Needs blockDim >= 512 and nreq * P * k' <= 256.
+__device__ void stage_select(const Plan& p, const State& st, int d, int P, int req0, int nreq,
+                             SelShared& sh) {
   const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
   const int kk = p.kk;
-  const int ncand = P * kk;
-
-  __shared__ uint64_t sh_wlist[NW][KMAX];
-  __shared__ float2 sh_wms[NW];
-  __shared__ uint64_t sh_rowkeys[16][KMAX];
-  __shared__ float sh_lse[16];
-  __shared__ uint64_t sh_ckey[256];
-  __shared__ int sh_rank[256];
-  __shared__ uint64_t sh_tkey[256];
-
-  // 1. merge the G slice lists of every frontier row of this request
-  const int wpr = NW / P;  // waves per row
-  const int prow = wave / wpr;
-  const int sub = wave - prow * wpr;
-  uint64_t list[KMAX];
-#pragma unroll
-  for (int i = 0; i < KMAX; ++i) list[i] = 0;
-  float m = kNegBig, s = 0.0f;
-  if (prow < P) {
-    const int grow = req * P + prow;
-    for (int g = sub * 64 + lane; g < p.G; g += wpr * 64) {
-      const size_t o = (size_t)g * p.rows_max + grow;
-      uint64_t other[KMAX];
-#pragma unroll
-      for (int i = 0; i < KMAX; ++i) other[i] = p.part_key[o * KMAX + i];
-      list_merge(list, other);
-      const float2 ms = p.part_ms[o];
-      lse_combine(m, s, ms.x, ms.y);
-    }
-  }
-#pragma unroll
-  for (int mask = 1; mask < 64; mask <<= 1) {
-    list_merge_xor(list, mask);
-    lse_combine_xor(m, s, mask);
-  }
-  if (lane == 0) {
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) sh_wlist[wave][i] = list[i];
-    sh_wms[wave] = make_float2(m, s);
-  }
-  __syncthreads();
-  if (prow < P && sub == 0) {
-    // lanes 0..wpr-1 of the row's first wave combine the row's waves
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) list[i] = lane < wpr ? sh_wlist[wave + lane][i] : 0;
-    m = lane < wpr ? sh_wms[wave + lane].x : kNegBig;
-    s = lane < wpr ? sh_wms[wave + lane].y : 0.0f;
-#pragma unroll
-    for (int mask = 1; mask < 16; mask <<= 1) {
-      list_merge_xor(list, mask);
-      lse_combine_xor(m, s, mask);
-    }
-    if (lane == 0) {
-#pragma unroll
-      for (int i = 0; i < KMAX; ++i) sh_rowkeys[prow][i] = list[i];
-      sh_lse[prow] = m + logf(s);
-    }
-  }
-  __syncthreads();
-
-  // 2. children of every frontier row, scored (Eq. 4), into the pool
+  const int per_req = P * kk;
+  const int ncand = nreq * per_req;
   const int nbase = d == 0 ? 1 : 1 + kk + (d - 1) * kk * kk;  // pool id of the first candidate
-  const size_t pb = (size_t)req * p.maxpool;
-  if (tid < ncand) {
-    const int pr = tid / kk;
-    const int j = tid - pr * kk;
-    const uint64_t ck = sh_rowkeys[pr][j];
-    // every row holds >= k' real keys (V >= k'); the clamp only keeps a
-    // corrupted key from indexing E out of bounds
-    const int tok = min(max(child_key_token(ck), 0), p.V - 1);
-    const float lp = child_key_value(ck) - sh_lse[pr];
-    const float score = p.front_score[req * kk + pr] + lp;
-    const int id = nbase + tid;
-    p.node_tok[pb + id] = tok;
-    p.node_par[pb + id] = p.front_node[req * kk + pr];
-    p.node_depth[pb + id] = d + 1;
-    p.node_score[pb + id] = score;
-    sh_ckey[tid] = node_key(score, d + 1, tok, pr);
-  }
-  const int cur = d & 1;
-  const int ncur = min(p.N, nbase);
-  const uint64_t* tk = p.top_key + ((size_t)cur * p.R + req) * p.N;
-  const int* tn = p.top_node + ((size_t)cur * p.R + req) * p.N;
-  if (tid >= 256 && tid < 256 + ncur) sh_tkey[tid - 256] = tk[tid - 256];
-  __syncthreads();
-
-  // 3. rank of every candidate within the layer (the layer order)
-  if (tid < ncand) {
-    const uint64_t key = sh_ckey[tid];
-    int rank = 0;
-    for (int c = 0; c < ncand; ++c) rank += sh_ckey[c] > key;
-    sh_rank[tid] = rank;
-  }
-  __syncthreads();
-
-  // 4. next frontier = the k' best candidates of the layer
   const bool more = d + 1 < p.B;
-  if (more && tid < ncand && sh_rank[tid] < kk) {
-    const int slot = sh_rank[tid];
-    const int pr = tid / kk;
-    const int id = nbase + tid;
-    const int tok = p.node_tok[pb + id];
-    const float score = p.node_score[pb + id];
-    p.front_node[req * kk + slot] = id;
-    p.front_tok[req * kk + slot] = tok;
-    p.front_score[req * kk + slot] = score;
+
+  int tok = 0;
+  float score = 0.0f;
+  if (tid < ncand) {
+    const int rq = tid / per_req;
+    const int ci = tid - rq * per_req;
+    const int pr = ci / kk;
+    const int j = ci - pr * kk;
+    const int req = req0 + rq;
+    const int lrow = rq * P + pr;
+    const uint64_t ck = sh.rowkeys[lrow][j];
+    // every row holds >= k' real keys (V >= k'); the clamp only keeps a
+    // corrupted key from indexing out of bounds
+    tok = min(max(child_key_token(ck), 0), p.V - 1);
+    const float lp = child_key_value(ck) - sh.lse[lrow];
+    score = st.front_score[req * kk + pr] + lp;
+    const size_t id = (size_t)req * p.maxpool + nbase + ci;
+    p.node_tok[id] = tok;
+    p.node_par[id] = st.front_node[req * kk + pr];
+    p.node_depth[id] = d + 1;
+    p.node_score[id] = score;
+    sh.ckey[tid] = node_key(score, d + 1, tok, pr);
+  }
+  __syncthreads();
+  // rank within the request's layer
+  if (tid < ncand) {
+    const int rq = tid / per_req;
+    sh.rank[tid] = count_greater(sh.ckey + rq * per_req, per_req, sh.ckey[tid]);
+  }
+  __syncthreads();
+  // next frontier (every frontier slot was read above, before the barriers)
+  if (more && tid < ncand && sh.rank[tid] < kk) {
+    const int rq = tid / per_req;
+    const int ci = tid - rq * per_req;
+    const int req = req0 + rq;
+    const int slot = sh.rank[tid];
+    st.front_node[req * kk + slot] = nbase + ci;
+    st.front_tok[req * kk + slot] = tok;
+    st.front_score[req * kk + slot] = score;
     if (p.t_token) {
       const size_t o = ((size_t)req * p.B + d + 1) * p.k + slot;
       p.t_token[o] = tok;
-      p.t_pslot[o] = pr;
+      p.t_pslot[o] = ci / kk;
       p.t_score[o] = score;
     }
   }
-
-  // 5. running global top-N: merge the sorted list with the ranked layer
-  const int nxt = cur ^ 1;
-  uint64_t* ok = p.top_key + ((size_t)nxt * p.R + req) * p.N;
-  int* on = p.top_node + ((size_t)nxt * p.R + req) * p.N;
-  if (tid < ncand) {
-    const uint64_t key = sh_ckey[tid];
-    int pos = sh_rank[tid];
-    for (int i = 0; i < ncur; ++i) pos += sh_tkey[i] > key;
-    if (pos < p.N) {
-      ok[pos] = key;
-      on[pos] = nbase + tid;
+  // running global top-N, one request at a time: every element's new
+  // position is its rank in the union (both sides are sorted), computed
+  // before any element moves
+  const int ncur = min(p.N, nbase);
+  for (int rq = 0; rq < nreq; ++rq) {
+    const int req = req0 + rq;
+    uint64_t* tk = st.top_key + (size_t)req * p.N;
+    int* tn = st.top_node + (size_t)req * p.N;
+    __syncthreads();
+    for (int i = tid; i < ncur; i += blockDim.x) sh.tkey[i] = tk[i];
+    __syncthreads();
+    int pos = p.N, node = 0;
+    uint64_t key = 0;
+    if (tid < per_req) {
+      const int c = rq * per_req + tid;
+      key = sh.ckey[c];
+      pos = sh.rank[c] + count_greater(sh.tkey, ncur, key);
+      node = nbase + tid;
+    } else if (tid >= 256 && tid < 256 + ncur) {
+      const int i = tid - 256;
+      key = sh.tkey[i];
+      pos = i + count_greater(sh.ckey + rq * per_req, per_req, key);
+      node = tn[i];
     }
-  } else if (tid >= 256 && tid < 256 + ncur) {
-    const int i = tid - 256;
-    const uint64_t key = sh_tkey[i];
-    int pos = i;
-    for (int c = 0; c < ncand; ++c) pos += sh_ckey[c] > key;
+    __syncthreads();
     if (pos < p.N) {
-      ok[pos] = key;
-      on[pos] = tn[i];
+      tk[pos] = key;
+      tn[pos] = node;
     }
   }
   __syncthreads();
+  if (more) write_activations(p, st, d + 1, req0, nreq);
+}
 
-  // 6. head input of the next frontier
-  if (more) {
-    const float* hd = p.h + ((size_t)req * p.B + d + 1) * p.r;
-    const int n = kk * p.r;
-    for (int e = tid; e < n; e += kSelectThreads) {
-      const int slot = e / p.r;
-      const int j = e - slot * p.r;
-      const int tok = p.front_tok[req * kk + slot];
-      // one element at a time: write_activation() with a stride over j
-      if (p.dtype) {
-        const uint16_t* er = (const uint16_t*)p.E + (size_t)tok * p.r;
-        ((uint16_t*)p.U)[(size_t)(req * kk + slot) * p.r + j] =
-            bf16_rne(silu_f32(__uint_as_float((uint32_t)er[j] << 16), hd[j]));
-      } else {
-        const float* er = (const float*)p.E + (size_t)tok * p.r;
-        ((float*)p.U)[(size_t)(req * kk + slot) * p.r + j] = silu_f32(er[j], hd[j]);
+// Merge the slice partials of the R*P rows (<= 16) of a stage into each row's
+// lse and top-k' children, one wave per row.  Only the k' slices whose best
+// key is among the k' largest slice maxima can hold one of the row's top-k'
+// keys, so just their lists are read.
+template <int KMAX, int WAVES>
+__device__ void merge_narrow(const Plan& p, int rows, SelShared& sh) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int kk = p.kk;
+  const int G = p.G;
+  for (int row = wave; row < rows; row += WAVES) {
+    float m = kNegBig, s = 0.0f;
+    uint64_t head[kHeadsPerLane];
+#pragma unroll
+    for (int i = 0; i < kHeadsPerLane; ++i) {
+      const int g = lane + 64 * i;
+      head[i] = 0;
+      if (g < G) {
+        const size_t o = (size_t)row * kSlicesMax + g;
+        const float2 ms = p.part_ms[o];
+        lse_combine(m, s, ms.x, ms.y);
+        head[i] = p.part_head[o];
       }
     }
+    {  // row lse: the wave's max, then the sum rescaled to it
+      const float M = wave_max_f32(m);
+      s = wave_sum_f32(s * exp2f((m - M) * kLog2e));
+      m = M;
+    }
+    // the k' largest slice maxima name the slices to read
+    int nwin = 0;
+#pragma unroll
+    for (int it = 0; it < KMAX; ++it) {
+      if (it < kk) {
+        uint64_t loc = 0;
+#pragma unroll
+        for (int i = 0; i < kHeadsPerLane; ++i) loc = head[i] > loc ? head[i] : loc;
+        const uint64_t best = wave_max_u64(loc);
+        if (best != 0) {
+          int who = -1;
+#pragma unroll
+          for (int i = 0; i < kHeadsPerLane; ++i)
+            if (head[i] == best) {
+              who = lane + 64 * i;
+              head[i] = 0;
+            }
+          const uint64_t hit = __ballot(who >= 0);
+          const int src = __ffsll((unsigned long long)hit) - 1;
+          const int g = __builtin_amdgcn_readlane(who, src);
+          if (lane == 0) sh.win[wave][nwin] = g;
+          ++nwin;
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    constexpr int CPL = (KMAX * KMAX + 63) / 64;
+    uint64_t cand[CPL];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      const int j = lane + 64 * q;
+      cand[q] = 0;
+      if (j < nwin * KMAX) {
+        const int g = sh.win[wave][j / KMAX];
+        cand[q] = p.part_key[((size_t)row * kSlicesMax + g) * KMAX + (j % KMAX)];
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < KMAX; ++it) {
+      if (it < kk) {
+        uint64_t loc = 0;
+#pragma unroll
+        for (int q = 0; q < CPL; ++q) loc = cand[q] > loc ? cand[q] : loc;
+        const uint64_t best = wave_max_u64(loc);
+#pragma unroll
+        for (int q = 0; q < CPL; ++q)
+          if (cand[q] == best) cand[q] = 0;
+        if (lane == 0) sh.rowkeys[row][it] = best;
+      }
+    }
+    if (lane == 0) sh.lse[row] = m + logf(s);
   }
+  __syncthreads();
 }
 
 // ---------------------------------------------------------------------------
@@ -522,21 +765,21 @@ __device__ void mask_rows(const int* par, int count, int N, uint32_t* out, uint3
 
 // Canonical order: depth ascending, then (parent's emitted index, token).
 // Level by level, every node of the level ranks itself among its level.
-__global__ __launch_bounds__(kEmitThreads) void emit_kernel(Plan p) {
+// Uses threads [0, 256) of the block (N <= 256); all threads must call it.
+__device__ void emit_request(const Plan& p, const State& st, int req) {
   __shared__ int sh_node[kEmitThreads], sh_emit[kEmitThreads], sh_par_emit[kEmitThreads];
   __shared__ uint64_t sh_skey[kEmitThreads];
   __shared__ int lev_cnt[64], lev_off[65], lev_fill[64], lev_mem[kEmitThreads];
   __shared__ uint32_t sh_words[kEmitThreads * (PCTREE_EMIT_MAX_N / 32)];
 
-  const int req = blockIdx.x;
   const int tid = threadIdx.x;
   const int kk = p.kk;
   const int pool = 1 + kk + (p.B - 1) * kk * kk;
   int count = min(p.N, pool);
   if (p.req_bad[req]) count = 0;
-  const int fin = p.B & 1;
   const size_t pb = (size_t)req * p.maxpool;
 
+  __syncthreads();
   if (tid < 64) {
     lev_cnt[tid] = 0;
     lev_fill[tid] = 0;
@@ -545,7 +788,7 @@ __global__ __launch_bounds__(kEmitThreads) void emit_kernel(Plan p) {
   int node = -1, dep = -1, tok = -1, pnode = -1;
   float score = 0.0f;
   if (tid < count) {
-    node = p.top_node[((size_t)fin * p.R + req) * p.N + tid];
+    node = st.top_node[(size_t)req * p.N + tid];
     dep = p.node_depth[pb + node];
     tok = p.node_tok[pb + node];
     pnode = p.node_par[pb + node];
@@ -607,9 +850,192 @@ __global__ __launch_bounds__(kEmitThreads) void emit_kernel(Plan p) {
   if (tid == 0) p.o_count[req] = count;
   if (p.o_mask) {
     __syncthreads();
-    mask_rows(sh_par_emit, count, p.N, p.o_mask + (size_t)req * p.N * ((p.N + 31) / 32),
-              sh_words, PCTREE_EMIT_MAX_N / 32);
+    if (tid < kEmitThreads)
+      mask_rows(sh_par_emit, count, p.N, p.o_mask + (size_t)req * p.N * ((p.N + 31) / 32),
+                sh_words, PCTREE_EMIT_MAX_N / 32);
   }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// narrow form: one persistent cooperative kernel per round
+// ---------------------------------------------------------------------------
+// Thread 0 of workgroup g waits until its own flag line flags[g * 64] reaches
+// `target` (one line per workgroup: a single word polled by every workgroup
+// would queue all polls at one memory channel).  It polls with relaxed loads
+// (an acquire load would invalidate the L2 on every poll) and acquires once at
+// the end.  Every wait is bounded by p.spin_ticks of the device wall clock; on
+// a timeout the workgroup raises the abort word and leaves the round, which
+// then ends without emission (count stays -1).
+__device__ int wait_flag(const Plan& p, int target) {
+  int* flag = p.flags + (size_t)blockIdx.x * kFlagStride;
+  const long long t0 = wall_clock64();
+  for (;;) {
+    if (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target) {
+      __atomic_thread_fence_agent_acquire();
+      return 1;
+    }
+    if (wall_clock64() - t0 > p.spin_ticks) {
+      __hip_atomic_store(p.sync + p.B, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return 0;
+    }
+    __builtin_amdgcn_s_sleep(2);
+  }
+}
+
+// Wait (thread 0) until the arrival counter of stage d has counted every
+// streaming workgroup, then acquire their partials.  Bounded like wait_flag.
+__device__ int wait_arrivals(const Plan& p, int d) {
+  int* cnt = p.sync + d;
+  const long long t0 = wall_clock64();
+  for (;;) {
+    if (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= p.G) {
+      __atomic_thread_fence_agent_acquire();
+      return 1;
+    }
+    if (wall_clock64() - t0 > p.spin_ticks) {
+      __hip_atomic_store(p.sync + p.B, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return 0;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+// Blocks [0, G) stream one V-slice each per stage; block G is the selector:
+// it keeps the frontier and the running top-N in LDS for the whole round,
+// waits for the G partials of a stage, merges and selects, writes the next
+// head input and raises every streaming block's flag; after the last stage it
+// emits the tree.  Synchronisation uses thread 0 of each block: stores by any
+// wave are ordered before its agent-scope release by the workgroup barrier,
+// and its agent-scope acquire is ordered before every wave's later loads by
+// the next barrier.
+template <int DT, int NCMAX, int KMAX>
+__global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
+  __shared__ int sh_go;
+  if (blockIdx.x < p.G) {
+    __shared__ HeadShared<KMAX, kRoundWaves> hsh;
+    const int slice = blockIdx.x;
+    for (int d = 0; d < p.B; ++d) {
+      if (d > 0) {
+        if (threadIdx.x == 0) sh_go = wait_flag(p, d);
+        __syncthreads();
+        if (!sh_go) return;
+      }
+      head_slice<DT, NCMAX, KMAX, kRoundWaves>(p, d, d == 0 ? 1 : p.kk, 0, slice, hsh);
+      __syncthreads();
+      if (threadIdx.x == 0)
+        __hip_atomic_fetch_add(p.sync + d, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return;
+  }
+
+  // the selector block
+  __shared__ SelShared ssh;
+  __shared__ int s_front_node[kNarrowRows], s_front_tok[kNarrowRows];
+  __shared__ float s_front_score[kNarrowRows];
+  extern __shared__ uint64_t s_top[];  // [R][N] keys, then [R][N] pool ids
+  const State st{s_front_node, s_front_tok, s_front_score, s_top,
+                 (int*)(s_top + (size_t)p.R * p.N)};
+  for (int req = threadIdx.x; req < p.R; req += blockDim.x) {
+    const int root = p.req_bad[req] ? 0 : p.root[req];
+    st.front_node[req * p.kk] = 0;
+    st.front_tok[req * p.kk] = root;
+    st.front_score[req * p.kk] = 0.0f;
+    st.top_key[(size_t)req * p.N] = node_key(0.0f, 0, root, 0);
+    st.top_node[(size_t)req * p.N] = 0;
+  }
+  for (int d = 0; d < p.B; ++d) {
+    const int P = d == 0 ? 1 : p.kk;
+    if (threadIdx.x == 0) sh_go = wait_arrivals(p, d);
+    __syncthreads();
+    if (!sh_go) return;
+    merge_narrow<KMAX, kRoundWaves>(p, p.R * P, ssh);
+    stage_select(p, st, d, P, 0, p.R, ssh);
+    if (d + 1 < p.B) {
+      __syncthreads();
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      for (int g = threadIdx.x; g < p.G; g += blockDim.x)
+        __hip_atomic_store(p.flags + (size_t)g * kFlagStride, d + 1, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      for (int req = 0; req < p.R; ++req) emit_request(p, st, req);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// wide form: per-stage head and select launches
+// ---------------------------------------------------------------------------
+template <int DT, int NCMAX, int KMAX>
+__global__ __launch_bounds__(kHeadThreads) void head_kernel(Plan p, int d, int P) {
+  __shared__ HeadShared<KMAX, kHeadThreads / 64> hsh;
+  head_slice<DT, NCMAX, KMAX, kHeadThreads / 64>(p, d, P, blockIdx.y, blockIdx.x, hsh);
+}
+
+// One WG per request: merge the G slice lists of its P rows (waves per row,
+// lanes per slice, then xor trees), then the shared stage selection.
+template <int KMAX>
+__global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, int P) {
+  constexpr int NW = kSelectThreads / 64;
+  __shared__ uint64_t sh_wlist[NW][KMAX];
+  __shared__ float2 sh_wms[NW];
+  __shared__ SelShared ssh;
+  const int req = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+
+  const int wpr = NW / P;  // waves per row
+  const int prow = wave / wpr;
+  const int sub = wave - prow * wpr;
+  uint64_t list[KMAX];
+#pragma unroll
+  for (int i = 0; i < KMAX; ++i) list[i] = 0;
+  float m = kNegBig, s = 0.0f;
+  if (prow < P) {
+    const int grow = req * P + prow;
+    for (int g = sub * 64 + lane; g < p.G; g += wpr * 64) {
+      const size_t o = (size_t)grow * kSlicesMax + g;
+      uint64_t other[KMAX];
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) other[i] = p.part_key[o * KMAX + i];
+      list_merge(list, other);
+      const float2 ms = p.part_ms[o];
+      lse_combine(m, s, ms.x, ms.y);
+    }
+  }
+#pragma unroll
+  for (int mask = 1; mask < 64; mask <<= 1) {
+    list_merge_xor(list, mask);
+    lse_combine_xor(m, s, mask);
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) sh_wlist[wave][i] = list[i];
+    sh_wms[wave] = make_float2(m, s);
+  }
+  __syncthreads();
+  if (prow < P && sub == 0) {
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) list[i] = lane < wpr ? sh_wlist[wave + lane][i] : 0;
+    m = lane < wpr ? sh_wms[wave + lane].x : kNegBig;
+    s = lane < wpr ? sh_wms[wave + lane].y : 0.0f;
+#pragma unroll
+    for (int mask = 1; mask < 16; mask <<= 1) {
+      list_merge_xor(list, mask);
+      lse_combine_xor(m, s, mask);
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) ssh.rowkeys[prow][i] = list[i];
+      ssh.lse[prow] = m + logf(s);
+    }
+  }
+  __syncthreads();
+  stage_select(p, global_state(p), d, P, req, 1, ssh);
+}
+
+__global__ __launch_bounds__(kEmitThreads) void emit_kernel(Plan p) {
+  emit_request(p, global_state(p), blockIdx.x);
 }
 
 __global__ __launch_bounds__(kMaskThreads) void mask_kernel(const int* parent, const int* count,
@@ -627,31 +1053,32 @@ __global__ __launch_bounds__(kMaskThreads) void mask_kernel(const int* parent, c
 // ---------------------------------------------------------------------------
 // dispatch
 // ---------------------------------------------------------------------------
-typedef void (*HeadFn)(Plan, int, int);
-typedef void (*SelectFn)(Plan, int, int);
+typedef void (*StageFn)(Plan, int, int);
+typedef void (*RoundFn)(Plan);
 
-template <int DT, int NCMAX>
-HeadFn head_for_kmax(int kmax) {
-  switch (kmax) {
-    case 1: return head_kernel<DT, NCMAX, 1>;
-    case 2: return head_kernel<DT, NCMAX, 2>;
-    case 4: return head_kernel<DT, NCMAX, 4>;
-    case 8: return head_kernel<DT, NCMAX, 8>;
-    default: return head_kernel<DT, NCMAX, 16>;
+#define PCTREE_KMAX_SWITCH(KERNEL, DT, NCMAX, kmax) \
+  switch (kmax) {                                   \
+    case 1: return KERNEL<DT, NCMAX, 1>;            \
+    case 2: return KERNEL<DT, NCMAX, 2>;            \
+    case 4: return KERNEL<DT, NCMAX, 4>;            \
+    case 8: return KERNEL<DT, NCMAX, 8>;            \
+    default: return KERNEL<DT, NCMAX, 16>;          \
   }
-}
 
-HeadFn head_fn(const Plan& p) {
-  if (p.dtype) {
-    if (p.nchunk <= 4) return head_for_kmax<1, 4>(p.kmax);
-    if (p.nchunk <= 8) return head_for_kmax<1, 8>(p.kmax);
-    return head_for_kmax<1, 16>(p.kmax);
-  }
-  if (p.nchunk <= 2) return head_for_kmax<0, 2>(p.kmax);
-  return head_for_kmax<0, 8>(p.kmax);
-}
+#define PCTREE_DISPATCH(KERNEL, p)                                    \
+  if ((p).dtype) {                                                    \
+    if ((p).nchunk <= 4) { PCTREE_KMAX_SWITCH(KERNEL, 1, 4, (p).kmax) } \
+    if ((p).nchunk <= 8) { PCTREE_KMAX_SWITCH(KERNEL, 1, 8, (p).kmax) } \
+    if ((p).nchunk <= 12) { PCTREE_KMAX_SWITCH(KERNEL, 1, 12, (p).kmax) } \
+    PCTREE_KMAX_SWITCH(KERNEL, 1, 16, (p).kmax)                       \
+  }                                                                   \
+  if ((p).nchunk <= 2) { PCTREE_KMAX_SWITCH(KERNEL, 0, 2, (p).kmax) } \
+  PCTREE_KMAX_SWITCH(KERNEL, 0, 8, (p).kmax)
 
-SelectFn select_fn(int kmax) {
+StageFn head_fn(const Plan& p) { PCTREE_DISPATCH(head_kernel, p) }
+RoundFn round_fn(const Plan& p) { PCTREE_DISPATCH(round_kernel, p) }
+
+StageFn select_fn(int kmax) {
   switch (kmax) {
     case 1: return select_kernel<1>;
     case 2: return select_kernel<2>;
@@ -661,26 +1088,80 @@ SelectFn select_fn(int kmax) {
   }
 }
 
+// Per-device facts for the persistent launch, queried once per device.
+struct DeviceInfo {
+  int cus = 0;
+  long long ticks_per_s = 0;
+};
+
+DeviceInfo device_info() {
+  static DeviceInfo cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return DeviceInfo{};
+  DeviceInfo& di = cache[dev];
+  if (di.cus == 0) {
+    int cus = 0, khz = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      cus = 0;
+    if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess) khz = 0;
+    di.ticks_per_s = (long long)(khz > 0 ? khz : 100000) * 1000;
+    di.cus = cus;
+  }
+  return di;
+}
+
 }  // namespace
 
-hipError_t launch_round(const Plan& p, hipStream_t st) {
+hipError_t launch_round(const Plan& p0, hipStream_t st) {
+  const bool narrow = p0.R * p0.kk <= kNarrowRows;
+  Plan p = p0;
+  DeviceInfo di;
+  RoundFn rfn = nullptr;
+  int fit = 0;
+  // selector LDS for the running top-N (keys + pool ids) of every request
+  const size_t smem = (size_t)p.R * p.N * (sizeof(uint64_t) + sizeof(int));
+  if (narrow) {
+    di = device_info();
+    rfn = round_fn(p);
+    if (di.cus < 2 ||
+        hipFuncSetAttribute((const void*)rfn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)smem) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&fit, (const void*)rfn, kRoundWaves * 64,
+                                                     smem) != hipSuccess)
+      fit = 0;
+  }
+  if (narrow && fit > 0) {
+    // one streaming slice per remaining CU (at most kSlicesMax) plus the
+    // selector block: every workgroup is resident at once
+    const int target = std::max(1, std::min(di.cus - 1, kSlicesMax));
+    p.tiles_per_slice = (p.ntiles + target - 1) / target;
+    p.G = (p.ntiles + p.tiles_per_slice - 1) / p.tiles_per_slice;
+    p.spin_ticks = 2 * di.ticks_per_s;  // a stage never legitimately waits 2 s
+    hipLaunchKernelGGL(prologue_kernel, dim3(p.R), dim3(kEmitThreads), 0, st, p);
+    void* args[] = {&p};
+    const bool prof = profile_on();
+    if (prof) profile_mark(st, "round_kernel");
+    const hipError_t e = hipLaunchCooperativeKernel((const void*)rfn, dim3(p.G + 1),
+                                                    dim3(kRoundWaves * 64), args, smem, st);
+    if (prof) profile_mark(st, "round_kernel");
+    if (e != hipSuccess) return e;
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(prologue_kernel, dim3(p.R), dim3(kEmitThreads), 0, st, p);
-  const HeadFn head = head_fn(p);
-  const SelectFn sel = select_fn(p.kmax);
+  const StageFn head = head_fn(p);
+  const StageFn sel = select_fn(p.kmax);
   for (int d = 0; d < p.B; ++d) {
     const int P = d == 0 ? 1 : p.kk;
     const int cb = (p.R * P + kTile - 1) / kTile;
     const bool prof = profile_on();
-    if (prof) profile_mark(st);
+    if (prof) profile_mark(st, "head_kernel");
     hipLaunchKernelGGL(head, dim3(p.G, cb), dim3(kHeadThreads), 0, st, p, d, P);
-    if (prof) profile_mark(st);
+    if (prof) profile_mark(st, "head_kernel");
     hipLaunchKernelGGL(sel, dim3(p.R), dim3(kSelectThreads), 0, st, p, d, P);
   }
   hipLaunchKernelGGL(emit_kernel, dim3(p.R), dim3(kEmitThreads), 0, st, p);
   return hipGetLastError();
 }
-
-const char* dominant_kernel_name() { return "head_kernel"; }
 
 hipError_t launch_mask(const int* parent, const int* count, int R, int N, uint32_t* mask,
                        hipStream_t st) {

@@ -14,6 +14,9 @@ constexpr int kHeadThreads = 256;   // 4 waves
 constexpr int kSelectThreads = 1024;
 constexpr int kEmitThreads = 256;
 constexpr int kMaskThreads = 256;
+constexpr int kRoundWaves = 8;       // waves per WG of the persistent round kernel
+constexpr int kNarrowRows = 16;      // frontier rows (R * k') one column block holds
+constexpr int kFlagStride = 64;      // ints between two workgroups' flag words (256 B)
 
 // Everything one round needs, passed by value to every kernel.
 struct Plan {
@@ -54,11 +57,16 @@ struct Plan {
   int* node_par;     // [R][maxpool] pool id of the parent
   int* node_depth;   // [R][maxpool]
   float* node_score; // [R][maxpool]
-  uint64_t* top_key; // [2][R][N] running global top-N (sorted, descending)
-  int* top_node;     // [2][R][N]
-  uint64_t* part_key;// [G][rows_max][kmax] per-slice candidate lists
-  float2* part_ms;   // [G][rows_max] per-slice (row max, sum of exp)
+  uint64_t* top_key; // [R][N] running global top-N (sorted, descending)
+  int* top_node;     // [R][N]
+  uint64_t* part_key;// [rows_max][kSlicesMax][kmax] per-slice candidate lists
+  uint64_t* part_head;// [rows_max][kSlicesMax] best key of each slice list
+  float2* part_ms;   // [rows_max][kSlicesMax] per-slice (row max, sum of exp)
   int* req_bad;      // [R] root token outside [0, V)
+  int* sync;         // [B + 1]: per-depth arrival counters, then the abort word of
+                     // the persistent round kernel
+  int* flags;        // [kSlicesMax * kFlagStride]: per-workgroup "stage ready" lines
+  long long spin_ticks;  // device wall-clock ticks a wait may last before aborting
 };
 
 // Workspace layout for a plan; offsets are 256-byte aligned.  With base ==
@@ -74,8 +82,7 @@ hipError_t launch_round(const Plan& p, hipStream_t stream);
 // Event bracketing of the dominant kernel (pctree_profile.hip): call
 // profile_mark() right before and right after each of its launches.
 bool profile_on();
-void profile_mark(hipStream_t stream);
-const char* dominant_kernel_name();
+void profile_mark(hipStream_t stream, const char* kernel);
 
 // Enqueue the standalone ancestor-mask kernel.
 hipError_t launch_mask(const int* parent, const int* count, int R, int N, uint32_t* mask,

@@ -15,6 +15,7 @@ struct Recorder {
   bool on = false;
   std::vector<hipEvent_t> pool;  // start/stop pairs, reused across enables
   size_t used = 0;               // events handed out since enabling
+  const char* kernel = "";       // name given by the last mark
 };
 
 Recorder& rec() {
@@ -36,10 +37,11 @@ hipEvent_t next_event() {
 
 bool profile_on() { return rec().on; }
 
-void profile_mark(hipStream_t stream) {
+void profile_mark(hipStream_t stream, const char* kernel) {
   Recorder& r = rec();
   std::lock_guard<std::mutex> g(r.mu);
   if (!r.on) return;
+  r.kernel = kernel;
   hipEvent_t e = next_event();
   if (e) (void)hipEventRecord(e, stream);
 }
@@ -73,7 +75,7 @@ pctree_status pctree_profile_read(double* total_ms, int64_t* launches, const cha
   }
   *total_ms = sum;
   *launches = (int64_t)pairs;
-  if (kernel) *kernel = dominant_kernel_name();
+  if (kernel) *kernel = r.kernel;
   r.used = 0;
   return PCTREE_OK;
 }
