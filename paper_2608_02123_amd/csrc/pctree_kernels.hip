@@ -213,6 +213,38 @@ __device__ __forceinline__ void list_merge_xor(uint64_t (&l)[K], int mask) {
   list_merge(l, o);
 }
 
+// Exchange with lane ^ 16 / lane ^ 32 on the VALU (v_permlane{16,32}_swap):
+// each returns {own, partner} in a lane-dependent order, which a symmetric
+// combine (list merge, lse combine) does not care about.
+template <int X>
+__device__ __forceinline__ void swap_pair(uint32_t v, uint32_t& a, uint32_t& b) {
+  if constexpr (X == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    a = r[0];
+    b = r[1];
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    a = r[0];
+    b = r[1];
+  }
+}
+
+template <int X, int K>
+__device__ __forceinline__ void list_merge_pair(uint64_t (&l)[K]) {
+  uint64_t a[K], b[K];
+#pragma unroll
+  for (int i = 0; i < K; ++i) {
+    uint32_t alo, blo, ahi, bhi;
+    swap_pair<X>((uint32_t)l[i], alo, blo);
+    swap_pair<X>((uint32_t)(l[i] >> 32), ahi, bhi);
+    a[i] = ((uint64_t)ahi << 32) | alo;
+    b[i] = ((uint64_t)bhi << 32) | blo;
+  }
+  list_merge(a, b);
+#pragma unroll
+  for (int i = 0; i < K; ++i) l[i] = a[i];
+}
+
 // Wave-wide reductions on DPP lane permutations (VALU latency, not the LDS
 // path of a shuffle): within each 16-lane row by quad permutes and mirrors,
 // then across rows by broadcasts of lanes 15 and 31; lane 63 ends with the
@@ -284,6 +316,16 @@ __device__ __forceinline__ void lse_combine_xor(float& m, float& s, int mask) {
   const float om = __shfl_xor(m, mask);
   const float os = __shfl_xor(s, mask);
   lse_combine(m, s, om, os);
+}
+
+template <int X>
+__device__ __forceinline__ void lse_combine_pair(float& m, float& s) {
+  uint32_t m0, m1, s0, s1;
+  swap_pair<X>(__float_as_uint(m), m0, m1);
+  swap_pair<X>(__float_as_uint(s), s0, s1);
+  m = __uint_as_float(m0);
+  s = __uint_as_float(s0);
+  lse_combine(m, s, __uint_as_float(m1), __uint_as_float(s1));
 }
 
 // ---------------------------------------------------------------------------
@@ -377,92 +419,195 @@ __device__ __forceinline__ float raw_to_f32(uint32_t r) {
   return __uint_as_float(DT ? r << 16 : r);
 }
 
+// Lane geometry of a head pass over one block of 16 frontier rows.
+struct HeadLane {
+  int lane, wave, col, grp, row, req, slot;
+  bool row_ok;
+  __device__ HeadLane(const Plan& p, int P, int cb) {
+    lane = threadIdx.x & 63;
+    wave = threadIdx.x >> 6;
+    col = lane & 15;
+    grp = lane >> 4;
+    row = cb * kTile + col;
+    row_ok = row < p.R * P;
+    req = row_ok ? row / P : 0;
+    slot = row_ok ? row - req * P : 0;
+  }
+};
+
+// B fragments: the head input u of this lane's frontier row.
+template <int DT, int NCMAX>
+__device__ __forceinline__ void load_bfrag(const Plan& p, const HeadLane& h, u32x4 (&b)[NCMAX]) {
+  constexpr int KC = DT ? 32 : 16;
+  constexpr int ESZ = DT ? 2 : 4;
+  const char* urow =
+      (const char*)p.U + ((size_t)(h.req * p.kk + h.slot) * p.r + h.grp * (KC / 4)) * ESZ;
+#pragma unroll
+  for (int c = 0; c < NCMAX; ++c) {
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (c < p.nchunk && h.row_ok) v = *(const u32x4*)(urow + (size_t)c * KC * ESZ);
+    b[c] = v;
+  }
+}
+
+// A fragments of tile t (16 tokens x r) for this lane.  No branch: the token
+// is clamped into the vocabulary (rows of tokens >= V are discarded later),
+// chunks past the rank re-read the last chunk and meet zero B fragments.
+template <int DT, int NCMAX>
+__device__ __forceinline__ void load_afrag(const Plan& p, const HeadLane& h, int t,
+                                           u32x4 (&a)[NCMAX]) {
+  constexpr int KC = DT ? 32 : 16;
+  constexpr int ESZ = DT ? 2 : 4;
+  const int tok = min(t * kTile + h.col, p.V - 1);
+  const char* wrow = (const char*)p.Wt + ((size_t)tok * p.r + h.grp * (KC / 4)) * ESZ;
+#pragma unroll
+  for (int c = 0; c < NCMAX; ++c)
+    a[c] = *(const u32x4*)(wrow + (size_t)min(c, p.nchunk - 1) * KC * ESZ);
+}
+
+// L_d of the four tokens of tile t this lane's C fragment holds (raw bits).
+template <int DT>
+__device__ __forceinline__ void load_lfrag(const Plan& p, const HeadLane& h, int d, int t,
+                                           uint32_t (&l)[4]) {
+  const size_t lrow = ((size_t)h.req * p.B + d) * p.V;
+  const int tb = t * kTile + h.grp * 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) l[i] = load_raw<DT>(p.L, lrow + min(tb + i, p.V - 1));
+}
+
+// Per-lane running state of a row: online (max, sum of exp) and top-KMAX keys.
+template <int KMAX>
+struct RowAcc {
+  float m, s;
+  uint64_t list[KMAX];
+  __device__ void init() {
+    m = kNegBig;
+    s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) list[i] = 0;
+  }
+};
+
+// One tile: Z = A B^T on MFMA, add L_d, fold the lane's four logits of its
+// row into the online logsumexp and the top-k list.
+template <int DT, int NCMAX, int KMAX>
+__device__ __forceinline__ void tile_step(const Plan& p, const HeadLane& h,
+                                          const u32x4 (&a)[NCMAX], const u32x4 (&b)[NCMAX],
+                                          const uint32_t (&l)[4], int t, RowAcc<KMAX>& r) {
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < NCMAX; ++c) acc = mfma_chunk<DT>(a[c], b[c], acc);
+  if (h.row_ok) {
+    const int tb = t * kTile + h.grp * 4;
+    float z[4];
+    float tmax = kNegBig;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      z[i] = tb + i < p.V ? acc[i] + raw_to_f32<DT>(l[i]) : kNegBig;
+      tmax = fmaxf(tmax, z[i]);
+    }
+    const float nm = fmaxf(r.m, tmax);
+    float ss = r.s * exp2f((r.m - nm) * kLog2e);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (tb + i < p.V) ss += exp2f((z[i] - nm) * kLog2e);
+    r.m = nm;
+    r.s = ss;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (tb + i < p.V) {
+        const uint64_t key = child_key(z[i], tb + i);
+        if (key > r.list[KMAX - 1]) list_insert(r.list, key);
+      }
+    }
+  }
+}
+
+// Reduce the lanes' row states over the workgroup and publish the slice's
+// partial of every row (best keys, their head, and (max, sum)).
+template <int KMAX, int WAVES>
+__device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h, int slice,
+                                                RowAcc<KMAX>& r, HeadShared<KMAX, WAVES>& sh) {
+  // rows live in lanes col, col+16, col+32, col+48 of every wave
+  list_merge_pair<16>(r.list);
+  lse_combine_pair<16>(r.m, r.s);
+  list_merge_pair<32>(r.list);
+  lse_combine_pair<32>(r.m, r.s);
+  if (h.grp == 0) {
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) sh.wl[h.wave][h.col][i] = r.list[i];
+    sh.wms[h.wave][h.col] = make_float2(r.m, r.s);
+  }
+  __syncthreads();
+  if (h.wave == 0) {
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) r.list[i] = sh.wl[h.grp][h.col][i];
+    r.m = sh.wms[h.grp][h.col].x;
+    r.s = sh.wms[h.grp][h.col].y;
+#pragma unroll
+    for (int w = h.grp + 4; w < WAVES; w += 4) {
+      uint64_t o[KMAX];
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) o[i] = sh.wl[w][h.col][i];
+      list_merge(r.list, o);
+      lse_combine(r.m, r.s, sh.wms[w][h.col].x, sh.wms[w][h.col].y);
+    }
+    list_merge_pair<16>(r.list);
+    lse_combine_pair<16>(r.m, r.s);
+    list_merge_pair<32>(r.list);
+    lse_combine_pair<32>(r.m, r.s);
+    if (h.grp == 0 && h.row_ok) {
+      // write-through (agent-coherent) stores: the arrival count that
+      // follows needs no L2 write-back
+      const size_t o = (size_t)h.row * kSlicesMax + slice;
+      uint64_t* dst = p.part_key + o * KMAX;
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i)
+        __hip_atomic_store(dst + i, r.list[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(p.part_head + o, r.list[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint64_t ms = ((uint64_t)__float_as_uint(r.s) << 32) | __float_as_uint(r.m);
+      __hip_atomic_store((uint64_t*)(p.part_ms + o), ms, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+// Count this block's arrival at stage d (thread 0; wave 0 wrote the
+// partial).  The partial was stored write-through; waiting for those stores
+// to complete before the relaxed add makes the data reach the coherence point
+// before the count does, without an L2 write-back of the whole cache.
+__device__ __forceinline__ void arrive(const Plan& p, int d) {
+  if (threadIdx.x < 64) {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    if (threadIdx.x == 0)
+      __hip_atomic_fetch_add(p.sync + d, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Stream one slice of W for one block of 16 frontier rows (multi-launch form):
+// the next tiles' loads are in flight while this one computes (three tiles in
+// registers up to rank 256, else two).  Prefetches are unconditional (clamped
+// to the slice's last tile, surplus ones are never processed) so that the
+// compiler's waits on the loads in flight stay partial.
 template <int DT, int NCMAX, int KMAX, int WAVES>
 __device__ __forceinline__ void head_slice(const Plan& p, int d, int P, int cb, int slice,
                                            HeadShared<KMAX, WAVES>& sh) {
-  constexpr int KC = DT ? 32 : 16;  // rank elements per chunk (16 bytes per lane group)
-  constexpr int ESZ = DT ? 2 : 4;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int col = lane & 15;
-  const int grp = lane >> 4;
-  const int rows = p.R * P;
-  const int row = cb * kTile + col;
-  const bool row_ok = row < rows;
-  const int req = row_ok ? row / P : 0;
-  const int slot = row_ok ? row - req * P : 0;
-  const int nc = p.nchunk;
-
+  const HeadLane h(p, P, cb);
   u32x4 bfrag[NCMAX];
-  {
-    const char* urow =
-        (const char*)p.U + ((size_t)(req * p.kk + slot) * p.r + grp * (KC / 4)) * ESZ;
-#pragma unroll
-    for (int c = 0; c < NCMAX; ++c) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (c < nc && row_ok) v = *(const u32x4*)(urow + (size_t)c * KC * ESZ);
-      bfrag[c] = v;
-    }
-  }
-  const size_t lrow = ((size_t)req * p.B + d) * p.V;
-  const char* wbase = (const char*)p.Wt + ((size_t)col * p.r + grp * (KC / 4)) * ESZ;
-
-  float m = kNegBig, s = 0.0f;
-  uint64_t list[KMAX];
-#pragma unroll
-  for (int i = 0; i < KMAX; ++i) list[i] = 0;
-
-  // No branch in the load or MFMA path (a branch makes the compiler wait for
-  // every load in flight): token indices are clamped into the vocabulary, and
-  // chunks past the rank re-read the last chunk in bounds and meet zero B
-  // fragments.  Rows of tokens >= V are discarded in the epilogue.
+  load_bfrag<DT, NCMAX>(p, h, bfrag);
+  RowAcc<KMAX> r;
+  r.init();
   auto load = [&](Tile<NCMAX>& T, int t) {
-    const int tokA = min(t * kTile + col, p.V - 1);
-    const char* wrow = wbase + ((size_t)tokA - col) * p.r * ESZ;
-#pragma unroll
-    for (int c = 0; c < NCMAX; ++c)
-      T.a[c] = *(const u32x4*)(wrow + (size_t)min(c, nc - 1) * KC * ESZ);
-    const int tb = t * kTile + grp * 4;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) T.l[i] = load_raw<DT>(p.L, lrow + min(tb + i, p.V - 1));
+    load_afrag<DT, NCMAX>(p, h, t, T.a);
+    load_lfrag<DT>(p, h, d, t, T.l);
   };
-
   auto process = [&](const Tile<NCMAX>& T, int t) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int c = 0; c < NCMAX; ++c) acc = mfma_chunk<DT>(T.a[c], bfrag[c], acc);
-    if (row_ok) {
-      const int tb = t * kTile + grp * 4;
-      float z[4];
-      float tmax = kNegBig;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        z[i] = tb + i < p.V ? acc[i] + raw_to_f32<DT>(T.l[i]) : kNegBig;
-        tmax = fmaxf(tmax, z[i]);
-      }
-      const float nm = fmaxf(m, tmax);
-      float ss = s * exp2f((m - nm) * kLog2e);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (tb + i < p.V) ss += exp2f((z[i] - nm) * kLog2e);
-      m = nm;
-      s = ss;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (tb + i < p.V) {
-          const uint64_t key = child_key(z[i], tb + i);
-          if (key > list[KMAX - 1]) list_insert(list, key);
-        }
-      }
-    }
+    tile_step<DT, NCMAX, KMAX>(p, h, T.a, bfrag, T.l, t, r);
   };
-
-  // software pipeline: the next tiles' loads are in flight while this one
-  // computes (three tiles in registers up to rank 256, else two).
-  // Prefetches are unconditional (clamped to the slice's last tile, surplus
-  // ones are never processed) so the compiler's waits stay partial.
   const int t1 = min((slice + 1) * p.tiles_per_slice, p.ntiles);
-  int t = slice * p.tiles_per_slice + wave;
+  int t = slice * p.tiles_per_slice + h.wave;
   Tile<NCMAX> TA, TB;
   load(TA, min(t, t1 - 1));
   if constexpr (NCMAX <= 8) {
@@ -492,43 +637,101 @@ __device__ __forceinline__ void head_slice(const Plan& p, int d, int P, int cb, 
       t += WAVES;
     }
   }
+  publish_partial<KMAX, WAVES>(p, h, slice, r, sh);
+}
 
-  // rows live in lanes col, col+16, col+32, col+48 of every wave
-  list_merge_xor(list, 16);
-  lse_combine_xor(m, s, 16);
-  list_merge_xor(list, 32);
-  lse_combine_xor(m, s, 32);
-  if (grp == 0) {
+__device__ int wait_flag(const Plan& p, int target);
+
+// Tiles a streaming block of the persistent kernel keeps on chip for the
+// whole round: RT per wave in registers and up to LTW per wave in LDS.
+// (64 VGPRs of resident A fragments per lane at most: more spills.)
+__host__ __device__ constexpr int resident_reg_tiles(int ncmax) {
+  return ncmax <= 2 ? 4 : (ncmax <= 4 ? 3 : (ncmax <= 8 ? 2 : 1));
+}
+__host__ __device__ constexpr int resident_lds_tiles_per_wave(int ncmax) {
+  return ncmax <= 4 ? 4 : (ncmax <= 8 ? 2 : 1);
+}
+
+// A streaming block of the persistent kernel.  W of its slice is read from
+// memory once per round: the first RT*WAVES tiles go to registers, the next
+// p.lds_tiles to LDS (stored in MFMA fragment order), and only the rest, if
+// any, is streamed at every stage.  Each stage then loads L_d before waiting
+// for the selector's release, reads the new head input and runs the tiles.
+template <int DT, int NCMAX, int KMAX>
+__device__ void stream_block(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, u32x4* wl,
+                             int& sh_go) {
+  constexpr int WAVES = kRoundWaves;
+  constexpr int RT = resident_reg_tiles(NCMAX);
+  constexpr int LTW = resident_lds_tiles_per_wave(NCMAX);
+  const int slice = blockIdx.x;
+  const int t0 = slice * p.tiles_per_slice;
+  const int t1 = min(t0 + p.tiles_per_slice, p.ntiles);
+  const int nreg = min(t1 - t0, RT * WAVES);
+  const int nlds = min(t1 - t0 - nreg, min(p.lds_tiles, LTW * WAVES));
+  const int lds0 = t0 + nreg;     // first LDS-resident tile
+  const int str0 = lds0 + nlds;   // first streamed tile
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+
+  {  // load the resident tiles (the lane geometry of A does not depend on rows)
+    const HeadLane h0(p, 1, 0);
+    u32x4 a[NCMAX];
+    for (int j = wave; j < nlds; j += WAVES) {
+      load_afrag<DT, NCMAX>(p, h0, lds0 + j, a);
 #pragma unroll
-    for (int i = 0; i < KMAX; ++i) sh.wl[wave][col][i] = list[i];
-    sh.wms[wave][col] = make_float2(m, s);
+      for (int c = 0; c < NCMAX; ++c) wl[((size_t)j * NCMAX + c) * 64 + lane] = a[c];
+    }
+  }
+  u32x4 areg[RT][NCMAX];
+  {
+    const HeadLane h0(p, 1, 0);
+#pragma unroll
+    for (int i = 0; i < RT; ++i) load_afrag<DT, NCMAX>(p, h0, min(t0 + wave + WAVES * i, t1 - 1), areg[i]);
   }
   __syncthreads();
-  if (wave == 0) {
+
+  for (int d = 0; d < p.B; ++d) {
+    const int P = d == 0 ? 1 : p.kk;
+    const HeadLane h(p, P, 0);
+    // frontier-independent loads before the wait
+    uint32_t lreg[RT][4], llds[LTW][4];
 #pragma unroll
-    for (int i = 0; i < KMAX; ++i) list[i] = sh.wl[grp][col][i];
-    m = sh.wms[grp][col].x;
-    s = sh.wms[grp][col].y;
+    for (int i = 0; i < RT; ++i) load_lfrag<DT>(p, h, d, min(t0 + wave + WAVES * i, t1 - 1), lreg[i]);
 #pragma unroll
-    for (int w = grp + 4; w < WAVES; w += 4) {
-      uint64_t o[KMAX];
-#pragma unroll
-      for (int i = 0; i < KMAX; ++i) o[i] = sh.wl[w][col][i];
-      list_merge(list, o);
-      lse_combine(m, s, sh.wms[w][col].x, sh.wms[w][col].y);
+    for (int q = 0; q < LTW; ++q)
+      load_lfrag<DT>(p, h, d, min(lds0 + wave + WAVES * q, t1 - 1), llds[q]);
+    if (d > 0) {
+      if (threadIdx.x == 0) sh_go = wait_flag(p, d);
+      __syncthreads();
+      if (!sh_go) return;
     }
-    list_merge_xor(list, 16);
-    lse_combine_xor(m, s, 16);
-    list_merge_xor(list, 32);
-    lse_combine_xor(m, s, 32);
-    if (grp == 0 && row_ok) {
-      const size_t o = (size_t)row * kSlicesMax + slice;
-      uint64_t* dst = p.part_key + o * KMAX;
+    u32x4 bfrag[NCMAX];
+    load_bfrag<DT, NCMAX>(p, h, bfrag);
+    RowAcc<KMAX> r;
+    r.init();
 #pragma unroll
-      for (int i = 0; i < KMAX; ++i) dst[i] = list[i];
-      p.part_head[o] = list[0];
-      p.part_ms[o] = make_float2(m, s);
+    for (int i = 0; i < RT; ++i) {
+      const int t = t0 + wave + WAVES * i;
+      if (t < lds0) tile_step<DT, NCMAX, KMAX>(p, h, areg[i], bfrag, lreg[i], t, r);
     }
+#pragma unroll
+    for (int q = 0; q < LTW; ++q) {
+      const int j = wave + WAVES * q;
+      if (j < nlds) {
+        u32x4 a[NCMAX];
+#pragma unroll
+        for (int c = 0; c < NCMAX; ++c) a[c] = wl[((size_t)j * NCMAX + c) * 64 + lane];
+        tile_step<DT, NCMAX, KMAX>(p, h, a, bfrag, llds[q], lds0 + j, r);
+      }
+    }
+    for (int t = str0 + wave; t < t1; t += WAVES) {
+      Tile<NCMAX> T;
+      load_afrag<DT, NCMAX>(p, h, t, T.a);
+      load_lfrag<DT>(p, h, d, t, T.l);
+      tile_step<DT, NCMAX, KMAX>(p, h, T.a, bfrag, T.l, t, r);
+    }
+    publish_partial<KMAX, WAVES>(p, h, slice, r, sh);
+    arrive(p, d);
   }
 }
 
@@ -912,20 +1115,12 @@ __device__ int wait_arrivals(const Plan& p, int d) {
 template <int DT, int NCMAX, int KMAX>
 __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   __shared__ int sh_go;
+  // dynamic LDS: the selector's running top-N ([R][N] keys, then [R][N] pool
+  // ids); the streaming blocks' resident W tiles from p.lds_tile_offset
+  extern __shared__ uint64_t s_dyn[];
   if (blockIdx.x < p.G) {
     __shared__ HeadShared<KMAX, kRoundWaves> hsh;
-    const int slice = blockIdx.x;
-    for (int d = 0; d < p.B; ++d) {
-      if (d > 0) {
-        if (threadIdx.x == 0) sh_go = wait_flag(p, d);
-        __syncthreads();
-        if (!sh_go) return;
-      }
-      head_slice<DT, NCMAX, KMAX, kRoundWaves>(p, d, d == 0 ? 1 : p.kk, 0, slice, hsh);
-      __syncthreads();
-      if (threadIdx.x == 0)
-        __hip_atomic_fetch_add(p.sync + d, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    stream_block<DT, NCMAX, KMAX>(p, hsh, (u32x4*)((char*)s_dyn + p.lds_tile_offset), sh_go);
     return;
   }
 
@@ -933,7 +1128,7 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   __shared__ SelShared ssh;
   __shared__ int s_front_node[kNarrowRows], s_front_tok[kNarrowRows];
   __shared__ float s_front_score[kNarrowRows];
-  extern __shared__ uint64_t s_top[];  // [R][N] keys, then [R][N] pool ids
+  uint64_t* s_top = s_dyn;
   const State st{s_front_node, s_front_tok, s_front_score, s_top,
                  (int*)(s_top + (size_t)p.R * p.N)};
   for (int req = threadIdx.x; req < p.R; req += blockDim.x) {
@@ -1076,6 +1271,12 @@ typedef void (*RoundFn)(Plan);
   PCTREE_KMAX_SWITCH(KERNEL, 0, 8, (p).kmax)
 
 StageFn head_fn(const Plan& p) { PCTREE_DISPATCH(head_kernel, p) }
+
+// NCMAX of the instantiation PCTREE_DISPATCH picks.
+int nchunk_max(const Plan& p) {
+  if (p.dtype) return p.nchunk <= 4 ? 4 : (p.nchunk <= 8 ? 8 : (p.nchunk <= 12 ? 12 : 16));
+  return p.nchunk <= 2 ? 2 : 8;
+}
 RoundFn round_fn(const Plan& p) { PCTREE_DISPATCH(round_kernel, p) }
 
 StageFn select_fn(int kmax) {
@@ -1118,24 +1319,41 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
   DeviceInfo di;
   RoundFn rfn = nullptr;
   int fit = 0;
-  // selector LDS for the running top-N (keys + pool ids) of every request
-  const size_t smem = (size_t)p.R * p.N * (sizeof(uint64_t) + sizeof(int));
+  size_t smem = 0;
   if (narrow) {
     di = device_info();
     rfn = round_fn(p);
-    if (di.cus < 2 ||
-        hipFuncSetAttribute((const void*)rfn, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)smem) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&fit, (const void*)rfn, kRoundWaves * 64,
-                                                     smem) != hipSuccess)
-      fit = 0;
-  }
-  if (narrow && fit > 0) {
     // one streaming slice per remaining CU (at most kSlicesMax) plus the
     // selector block: every workgroup is resident at once
     const int target = std::max(1, std::min(di.cus - 1, kSlicesMax));
     p.tiles_per_slice = (p.ntiles + target - 1) / target;
     p.G = (p.ntiles + p.tiles_per_slice - 1) / p.tiles_per_slice;
+    // dynamic LDS: the selector's top-N, then as many resident W tiles as fit
+    const int ncmax = nchunk_max(p);
+    const size_t top = ((size_t)p.R * p.N * (sizeof(uint64_t) + sizeof(int)) + 255) & ~(size_t)255;
+    const size_t tile_bytes = (size_t)ncmax * 64 * 16;
+    hipFuncAttributes attr{};
+    int lds_max = 0;
+    int dev = 0;
+    if (di.cus >= 2 && hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) ==
+            hipSuccess &&
+        hipFuncGetAttributes(&attr, (const void*)rfn) == hipSuccess) {
+      const long room = (long)lds_max - (long)attr.sharedSizeBytes - (long)top - 1024;
+      const int want = std::max(0, p.tiles_per_slice - resident_reg_tiles(ncmax) * kRoundWaves);
+      const int cap = resident_lds_tiles_per_wave(ncmax) * kRoundWaves;
+      p.lds_tiles = room > 0 ? (int)std::min<long>({room / (long)tile_bytes, (long)want, (long)cap})
+                             : 0;
+      p.lds_tile_offset = (int)top;
+      smem = top + (size_t)p.lds_tiles * tile_bytes;
+      if (hipFuncSetAttribute((const void*)rfn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)smem) != hipSuccess ||
+          hipOccupancyMaxActiveBlocksPerMultiprocessor(&fit, (const void*)rfn, kRoundWaves * 64,
+                                                       smem) != hipSuccess)
+        fit = 0;
+    }
+  }
+  if (narrow && fit > 0) {
     p.spin_ticks = 2 * di.ticks_per_s;  // a stage never legitimately waits 2 s
     hipLaunchKernelGGL(prologue_kernel, dim3(p.R), dim3(kEmitThreads), 0, st, p);
     void* args[] = {&p};

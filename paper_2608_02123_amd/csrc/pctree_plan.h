@@ -67,6 +67,8 @@ struct Plan {
                      // the persistent round kernel
   int* flags;        // [kSlicesMax * kFlagStride]: per-workgroup "stage ready" lines
   long long spin_ticks;  // device wall-clock ticks a wait may last before aborting
+  int lds_tiles;         // W tiles a streaming block keeps in LDS for the whole round
+  int lds_tile_offset;   // byte offset of those tiles in the dynamic LDS
 };
 
 // Workspace layout for a plan; offsets are 256-byte aligned.  With base ==
