@@ -131,7 +131,6 @@ size_t carve_workspace(Plan& p, char* base) {
   p.top_key = (uint64_t*)take(R * p.N * sizeof(uint64_t));
   p.top_node = (int*)take(R * p.N * sizeof(int));
   p.part_key = (uint64_t*)take((size_t)kSlicesMax * p.rows_max * p.kmax * sizeof(uint64_t));
-  p.part_head = (uint64_t*)take((size_t)kSlicesMax * p.rows_max * sizeof(uint64_t));
   p.part_ms = (float2*)take((size_t)kSlicesMax * p.rows_max * sizeof(float2));
   p.req_bad = (int*)take(R * sizeof(int));
   p.sync = (int*)take((size_t)(p.B + 1) * sizeof(int));

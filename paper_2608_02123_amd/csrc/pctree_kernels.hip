@@ -45,7 +45,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegBig = -3.0e38f;  // "no value yet" for running maxima
-constexpr int kHeadsPerLane = kSlicesMax / 64;
 
 __device__ __forceinline__ void __atomic_thread_fence_agent_acquire() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
@@ -524,7 +523,7 @@ __device__ __forceinline__ void tile_step(const Plan& p, const HeadLane& h,
 }
 
 // Reduce the lanes' row states over the workgroup and publish the slice's
-// partial of every row (best keys, their head, and (max, sum)).
+// partial of every row (best keys and (max, sum)).
 template <int KMAX, int WAVES>
 __device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h, int slice,
                                                 RowAcc<KMAX>& r, HeadShared<KMAX, WAVES>& sh) {
@@ -564,7 +563,6 @@ __device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h
 #pragma unroll
       for (int i = 0; i < KMAX; ++i)
         __hip_atomic_store(dst + i, r.list[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(p.part_head + o, r.list[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       const uint64_t ms = ((uint64_t)__float_as_uint(r.s) << 32) | __float_as_uint(r.m);
       __hip_atomic_store((uint64_t*)(p.part_ms + o), ms, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
@@ -758,7 +756,6 @@ __device__ __forceinline__ int count_greater(const uint64_t* keys, int n, uint64
 struct SelShared {
   uint64_t rowkeys[kNarrowRows][16];  // top-k' children (child keys) of each row
   float lse[kNarrowRows];
-  int win[kRoundWaves][16];           // slices holding a row's top-k' (per-wave scratch)
   __attribute__((aligned(16))) uint64_t ckey[256];  // node keys of the stage's candidates
   int rank[256];
   __attribute__((aligned(16))) uint64_t tkey[PCTREE_EMIT_MAX_N];  // a request's top-N keys
@@ -859,27 +856,40 @@ __device__ void stage_select(const Plan& p, const State& st, int d, int P, int r
 }
 
 // Merge the slice partials of the R*P rows (<= 16) of a stage into each row's
-// lse and top-k' children, one wave per row.  Only the k' slices whose best
-// key is among the k' largest slice maxima can hold one of the row's top-k'
-// keys, so just their lists are read.
+// lse and top-k' children, one wave per row.  Every lane loads the complete
+// lists of its slices in one batch (one memory round trip), merges them into
+// one sorted list, and k' rounds of a wave-wide maximum pop the row's best
+// keys (the lane holding the winner shifts its list).
 template <int KMAX, int WAVES>
 __device__ void merge_narrow(const Plan& p, int rows, SelShared& sh) {
+  constexpr int CH = KMAX >= 16 ? 2 : (KMAX >= 8 ? 4 : 8);  // slices per lane per batch
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int kk = p.kk;
   const int G = p.G;
   for (int row = wave; row < rows; row += WAVES) {
     float m = kNegBig, s = 0.0f;
-    uint64_t head[kHeadsPerLane];
+    uint64_t acc[KMAX];
 #pragma unroll
-    for (int i = 0; i < kHeadsPerLane; ++i) {
-      const int g = lane + 64 * i;
-      head[i] = 0;
-      if (g < G) {
-        const size_t o = (size_t)row * kSlicesMax + g;
-        const float2 ms = p.part_ms[o];
-        lse_combine(m, s, ms.x, ms.y);
-        head[i] = p.part_head[o];
+    for (int i = 0; i < KMAX; ++i) acc[i] = 0;
+    const uint64_t* keys = p.part_key + (size_t)row * kSlicesMax * KMAX;
+    const float2* mss = p.part_ms + (size_t)row * kSlicesMax;
+    for (int base = 0; base < G; base += 64 * CH) {
+      uint64_t lst[CH][KMAX];
+      float2 ms[CH];
+#pragma unroll
+      for (int c = 0; c < CH; ++c) {
+        const int g = min(base + lane + 64 * c, G - 1);
+#pragma unroll
+        for (int i = 0; i < KMAX; ++i) lst[c][i] = keys[(size_t)g * KMAX + i];
+        ms[c] = mss[g];
+      }
+#pragma unroll
+      for (int c = 0; c < CH; ++c) {
+        if (base + lane + 64 * c < G) {
+          list_merge(acc, lst[c]);
+          lse_combine(m, s, ms[c].x, ms[c].y);
+        }
       }
     }
     {  // row lse: the wave's max, then the sum rescaled to it
@@ -887,53 +897,15 @@ __device__ void merge_narrow(const Plan& p, int rows, SelShared& sh) {
       s = wave_sum_f32(s * exp2f((m - M) * kLog2e));
       m = M;
     }
-    // the k' largest slice maxima name the slices to read
-    int nwin = 0;
 #pragma unroll
     for (int it = 0; it < KMAX; ++it) {
       if (it < kk) {
-        uint64_t loc = 0;
+        const uint64_t best = wave_max_u64(acc[0]);
+        if (acc[0] == best) {
 #pragma unroll
-        for (int i = 0; i < kHeadsPerLane; ++i) loc = head[i] > loc ? head[i] : loc;
-        const uint64_t best = wave_max_u64(loc);
-        if (best != 0) {
-          int who = -1;
-#pragma unroll
-          for (int i = 0; i < kHeadsPerLane; ++i)
-            if (head[i] == best) {
-              who = lane + 64 * i;
-              head[i] = 0;
-            }
-          const uint64_t hit = __ballot(who >= 0);
-          const int src = __ffsll((unsigned long long)hit) - 1;
-          const int g = __builtin_amdgcn_readlane(who, src);
-          if (lane == 0) sh.win[wave][nwin] = g;
-          ++nwin;
+          for (int i = 0; i + 1 < KMAX; ++i) acc[i] = acc[i + 1];
+          acc[KMAX - 1] = 0;
         }
-      }
-    }
-    __builtin_amdgcn_wave_barrier();
-    constexpr int CPL = (KMAX * KMAX + 63) / 64;
-    uint64_t cand[CPL];
-#pragma unroll
-    for (int q = 0; q < CPL; ++q) {
-      const int j = lane + 64 * q;
-      cand[q] = 0;
-      if (j < nwin * KMAX) {
-        const int g = sh.win[wave][j / KMAX];
-        cand[q] = p.part_key[((size_t)row * kSlicesMax + g) * KMAX + (j % KMAX)];
-      }
-    }
-#pragma unroll
-    for (int it = 0; it < KMAX; ++it) {
-      if (it < kk) {
-        uint64_t loc = 0;
-#pragma unroll
-        for (int q = 0; q < CPL; ++q) loc = cand[q] > loc ? cand[q] : loc;
-        const uint64_t best = wave_max_u64(loc);
-#pragma unroll
-        for (int q = 0; q < CPL; ++q)
-          if (cand[q] == best) cand[q] = 0;
         if (lane == 0) sh.rowkeys[row][it] = best;
       }
     }
@@ -1108,10 +1080,12 @@ __device__ int wait_arrivals(const Plan& p, int d) {
 // it keeps the frontier and the running top-N in LDS for the whole round,
 // waits for the G partials of a stage, merges and selects, writes the next
 // head input and raises every streaming block's flag; after the last stage it
-// emits the tree.  Synchronisation uses thread 0 of each block: stores by any
-// wave are ordered before its agent-scope release by the workgroup barrier,
-// and its agent-scope acquire is ordered before every wave's later loads by
-// the next barrier.
+// emits the tree.  Slice partials are stored write-through at agent scope and
+// a streaming block waits for those stores to complete before it counts its
+// arrival; the selector publishes the head inputs with an agent-scope release
+// before the flags.  A consumer's thread 0 polls with relaxed loads and
+// acquires once, ordered before every wave's later loads by the next
+// workgroup barrier.
 template <int DT, int NCMAX, int KMAX>
 __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   __shared__ int sh_go;

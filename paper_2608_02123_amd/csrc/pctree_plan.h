@@ -60,7 +60,6 @@ struct Plan {
   uint64_t* top_key; // [R][N] running global top-N (sorted, descending)
   int* top_node;     // [R][N]
   uint64_t* part_key;// [rows_max][kSlicesMax][kmax] per-slice candidate lists
-  uint64_t* part_head;// [rows_max][kSlicesMax] best key of each slice list
   float2* part_ms;   // [rows_max][kSlicesMax] per-slice (row max, sum of exp)
   int* req_bad;      // [R] root token outside [0, V)
   int* sync;         // [B + 1]: per-depth arrival counters, then the abort word of
