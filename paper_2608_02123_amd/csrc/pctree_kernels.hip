@@ -419,18 +419,34 @@ __device__ __forceinline__ float raw_to_f32(uint32_t r) {
 }
 
 // Lane geometry of a head pass over one block of 16 frontier rows.
+// With `fold` (at most 8 frontier rows) the C fragments of two tiles share
+// the 16 columns: columns 0..7 keep the first tile's rows, columns 8..15 take
+// the second tile's (moved up by 8), so that every lane holds a live row.  B
+// columns (the frontier rows fed to the MFMA) are unaffected.
 struct HeadLane {
-  int lane, wave, col, grp, row, req, slot;
+  int lane, wave, col, grp;
+  int row, req, slot;  // the frontier row whose logits this lane holds
   bool row_ok;
-  __device__ HeadLane(const Plan& p, int P, int cb) {
+  int half;            // which tile of a folded pair (0 without fold)
+  bool lead;           // the lane that publishes its row (first of a folded pair)
+  int b_req, b_slot;   // the frontier row of this lane's B column
+  bool b_ok;
+  __device__ HeadLane(const Plan& p, int P, int cb, bool fold = false) {
     lane = threadIdx.x & 63;
     wave = threadIdx.x >> 6;
     col = lane & 15;
     grp = lane >> 4;
-    row = cb * kTile + col;
-    row_ok = row < p.R * P;
+    const int nrows = p.R * P;
+    const int bcol = cb * kTile + col;
+    b_ok = bcol < nrows;
+    b_req = b_ok ? bcol / P : 0;
+    b_slot = b_ok ? bcol - b_req * P : 0;
+    row = cb * kTile + (fold ? (col & 7) : col);
+    row_ok = row < nrows;
     req = row_ok ? row / P : 0;
     slot = row_ok ? row - req * P : 0;
+    half = fold ? (col >> 3) : 0;
+    lead = !fold || col < 8;
   }
 };
 
@@ -440,11 +456,11 @@ __device__ __forceinline__ void load_bfrag(const Plan& p, const HeadLane& h, u32
   constexpr int KC = DT ? 32 : 16;
   constexpr int ESZ = DT ? 2 : 4;
   const char* urow =
-      (const char*)p.U + ((size_t)(h.req * p.kk + h.slot) * p.r + h.grp * (KC / 4)) * ESZ;
+      (const char*)p.U + ((size_t)(h.b_req * p.kk + h.b_slot) * p.r + h.grp * (KC / 4)) * ESZ;
 #pragma unroll
   for (int c = 0; c < NCMAX; ++c) {
     u32x4 v = {0u, 0u, 0u, 0u};
-    if (c < p.nchunk && h.row_ok) v = *(const u32x4*)(urow + (size_t)c * KC * ESZ);
+    if (c < p.nchunk && h.b_ok) v = *(const u32x4*)(urow + (size_t)c * KC * ESZ);
     b[c] = v;
   }
 }
@@ -487,16 +503,13 @@ struct RowAcc {
   }
 };
 
-// One tile: Z = A B^T on MFMA, add L_d, fold the lane's four logits of its
-// row into the online logsumexp and the top-k list.
-template <int DT, int NCMAX, int KMAX>
-__device__ __forceinline__ void tile_step(const Plan& p, const HeadLane& h,
-                                          const u32x4 (&a)[NCMAX], const u32x4 (&b)[NCMAX],
-                                          const uint32_t (&l)[4], int t, RowAcc<KMAX>& r) {
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int c = 0; c < NCMAX; ++c) acc = mfma_chunk<DT>(a[c], b[c], acc);
-  if (h.row_ok) {
+// The lane's four logits of tile t (C fragment + L_d), folded into its row's
+// online logsumexp and top-k list when `ok`.
+template <int DT, int KMAX>
+__device__ __forceinline__ void tile_epilogue(const Plan& p, const HeadLane& h, f32x4 acc,
+                                              const uint32_t (&l)[4], int t, bool ok,
+                                              RowAcc<KMAX>& r) {
+  if (ok) {
     const int tb = t * kTile + h.grp * 4;
     float z[4];
     float tmax = kNegBig;
@@ -522,11 +535,72 @@ __device__ __forceinline__ void tile_step(const Plan& p, const HeadLane& h,
   }
 }
 
+// One tile: Z = A B^T on MFMA, then the epilogue.
+template <int DT, int NCMAX, int KMAX>
+__device__ __forceinline__ void tile_step(const Plan& p, const HeadLane& h,
+                                          const u32x4 (&a)[NCMAX], const u32x4 (&b)[NCMAX],
+                                          const uint32_t (&l)[4], int t, RowAcc<KMAX>& r) {
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < NCMAX; ++c) acc = mfma_chunk<DT>(a[c], b[c], acc);
+  tile_epilogue<DT, KMAX>(p, h, acc, l, t, h.row_ok, r);
+}
+
+// Two tiles on two independent MFMA chains; the second tile's C fragment is
+// moved into columns 8..15 (DPP row_shr:8 onto banks 2-3 of every row), then
+// one epilogue covers both.  t is the lane's own tile (ta or tb by half).
+template <int DT, int NCMAX, int KMAX>
+__device__ __forceinline__ void tile_pair_step(const Plan& p, const HeadLane& h,
+                                               const u32x4 (&a0)[NCMAX], const u32x4 (&a1)[NCMAX],
+                                               const u32x4 (&b)[NCMAX], const uint32_t (&l)[4],
+                                               int t, bool ok, RowAcc<KMAX>& r) {
+  f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < NCMAX; ++c) {
+    c0 = mfma_chunk<DT>(a0[c], b[c], c0);
+    c1 = mfma_chunk<DT>(a1[c], b[c], c1);
+  }
+  f32x4 acc;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    acc[i] = __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(c0[i]), __float_as_int(c1[i]),
+                                                        0x118, 0xF, 0xC, false));
+  tile_epilogue<DT, KMAX>(p, h, acc, l, t, ok && h.row_ok, r);
+}
+
+// tile_pair_step on two LDS-resident tiles (fragment order), reading each
+// rank chunk right before its MFMA so that only two chunks are live.
+template <int DT, int NCMAX, int KMAX>
+__device__ __forceinline__ void lds_pair_step(const Plan& p, const HeadLane& h, const u32x4* w0,
+                                              const u32x4* w1, const u32x4 (&b)[NCMAX],
+                                              const uint32_t (&l)[4], int t, bool ok,
+                                              RowAcc<KMAX>& r) {
+  f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < NCMAX; ++c) {
+    c0 = mfma_chunk<DT>(w0[c * 64], b[c], c0);
+    c1 = mfma_chunk<DT>(w1[c * 64], b[c], c1);
+  }
+  f32x4 acc;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    acc[i] = __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(c0[i]), __float_as_int(c1[i]),
+                                                        0x118, 0xF, 0xC, false));
+  tile_epilogue<DT, KMAX>(p, h, acc, l, t, ok && h.row_ok, r);
+}
+
 // Reduce the lanes' row states over the workgroup and publish the slice's
 // partial of every row (best keys and (max, sum)).
-template <int KMAX, int WAVES>
+template <int KMAX, int WAVES, bool FOLD = false>
 __device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h, int slice,
                                                 RowAcc<KMAX>& r, HeadShared<KMAX, WAVES>& sh) {
+  if constexpr (FOLD) {  // the two lanes of a folded row: col and col ^ 8 (DPP row_ror:8)
+    uint64_t o[KMAX];
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) o[i] = dpp64<0x128, 0xF>(r.list[i]);
+    list_merge(r.list, o);
+    lse_combine(r.m, r.s, dppf<0x128, 0xF>(r.m, kNegBig), dppf<0x128, 0xF>(r.s, 0.0f));
+  }
   // rows live in lanes col, col+16, col+32, col+48 of every wave
   list_merge_pair<16>(r.list);
   lse_combine_pair<16>(r.m, r.s);
@@ -555,7 +629,7 @@ __device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h
     lse_combine_pair<16>(r.m, r.s);
     list_merge_pair<32>(r.list);
     lse_combine_pair<32>(r.m, r.s);
-    if (h.grp == 0 && h.row_ok) {
+    if (h.grp == 0 && h.row_ok && h.lead) {
       // write-through (agent-coherent) stores: the arrival count that
       // follows needs no L2 write-back
       const size_t o = (size_t)h.row * kSlicesMax + slice;
@@ -729,6 +803,102 @@ __device__ void stream_block(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, u
       tile_step<DT, NCMAX, KMAX>(p, h, T.a, bfrag, T.l, t, r);
     }
     publish_partial<KMAX, WAVES>(p, h, slice, r, sh);
+    arrive(p, d);
+  }
+}
+
+// stream_block for at most 8 frontier rows: tiles go through the MFMA in
+// pairs whose C fragments are folded into one set of 16 columns (see
+// HeadLane), so every lane's epilogue works on a live row.
+template <int DT, int NCMAX, int KMAX>
+__device__ void stream_block_fold(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, u32x4* wl,
+                                  int& sh_go) {
+  constexpr int WAVES = kRoundWaves;
+  constexpr int RT = resident_reg_tiles(NCMAX);
+  constexpr int LTW = resident_lds_tiles_per_wave(NCMAX);
+  constexpr int RP = (RT + 1) / 2;   // register-resident pairs per wave
+  constexpr int LP = (LTW + 1) / 2;  // LDS-resident pairs per wave
+  const int slice = blockIdx.x;
+  const int t0 = slice * p.tiles_per_slice;
+  const int t1 = min(t0 + p.tiles_per_slice, p.ntiles);
+  const int nreg = min(t1 - t0, RT * WAVES);
+  const int nlds = min(t1 - t0 - nreg, min(p.lds_tiles, LTW * WAVES));
+  const int lds0 = t0 + nreg;
+  const int str0 = lds0 + nlds;
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+
+  {
+    const HeadLane h0(p, 1, 0);
+    u32x4 a[NCMAX];
+    for (int j = wave; j < nlds; j += WAVES) {
+      load_afrag<DT, NCMAX>(p, h0, lds0 + j, a);
+#pragma unroll
+      for (int c = 0; c < NCMAX; ++c) wl[((size_t)j * NCMAX + c) * 64 + lane] = a[c];
+    }
+  }
+  u32x4 areg[RT][NCMAX];
+  {
+    const HeadLane h0(p, 1, 0);
+#pragma unroll
+    for (int i = 0; i < RT; ++i) load_afrag<DT, NCMAX>(p, h0, min(t0 + wave + WAVES * i, t1 - 1), areg[i]);
+  }
+  __syncthreads();
+
+  for (int d = 0; d < p.B; ++d) {
+    const int P = d == 0 ? 1 : p.kk;
+    const HeadLane h(p, P, 0, true);
+    // L_d of the lane's own tile of every resident pair, before the wait
+    uint32_t lreg[RP][4], llds[LP][4];
+#pragma unroll
+    for (int q = 0; q < RP; ++q)
+      load_lfrag<DT>(p, h, d, min(t0 + wave + WAVES * (2 * q + h.half), t1 - 1), lreg[q]);
+#pragma unroll
+    for (int q = 0; q < LP; ++q)
+      load_lfrag<DT>(p, h, d, min(lds0 + wave + WAVES * (2 * q + h.half), t1 - 1), llds[q]);
+    if (d > 0) {
+      if (threadIdx.x == 0) sh_go = wait_flag(p, d);
+      __syncthreads();
+      if (!sh_go) return;
+    }
+    u32x4 bfrag[NCMAX];
+    load_bfrag<DT, NCMAX>(p, h, bfrag);
+    RowAcc<KMAX> r;
+    r.init();
+#pragma unroll
+    for (int q = 0; q < RP; ++q) {
+      const int i1 = min(2 * q + 1, RT - 1);
+      const int ta = t0 + wave + WAVES * (2 * q);
+      const int tb = t0 + wave + WAVES * (2 * q + 1);
+      const bool okb = 2 * q + 1 < RT && tb < lds0;
+      if (ta < lds0)
+        tile_pair_step<DT, NCMAX, KMAX>(p, h, areg[2 * q], areg[i1], bfrag, lreg[q],
+                                        h.half ? tb : ta, h.half ? okb : true, r);
+    }
+#pragma unroll
+    for (int q = 0; q < LP; ++q) {
+      const int ja = wave + WAVES * (2 * q);
+      const int jb = wave + WAVES * (2 * q + 1);
+      if (ja < nlds) {
+        const bool okb = 2 * q + 1 < LTW && jb < nlds;
+        const int jl = okb ? jb : ja;
+        lds_pair_step<DT, NCMAX, KMAX>(p, h, wl + (size_t)ja * NCMAX * 64 + lane,
+                                       wl + (size_t)jl * NCMAX * 64 + lane, bfrag, llds[q],
+                                       lds0 + (h.half ? jb : ja), h.half ? okb : true, r);
+      }
+    }
+    for (int ta = str0 + wave; ta < t1; ta += 2 * WAVES) {
+      const int tb = ta + WAVES;
+      const bool okb = tb < t1;
+      const int tl = h.half && okb ? tb : ta;
+      u32x4 a0[NCMAX], a1[NCMAX];
+      uint32_t l[4];
+      load_afrag<DT, NCMAX>(p, h, ta, a0);
+      load_afrag<DT, NCMAX>(p, h, okb ? tb : ta, a1);
+      load_lfrag<DT>(p, h, d, tl, l);
+      tile_pair_step<DT, NCMAX, KMAX>(p, h, a0, a1, bfrag, l, tl, h.half ? okb : true, r);
+    }
+    publish_partial<KMAX, WAVES, true>(p, h, slice, r, sh);
     arrive(p, d);
   }
 }
@@ -1086,7 +1256,7 @@ __device__ int wait_arrivals(const Plan& p, int d) {
 // before the flags.  A consumer's thread 0 polls with relaxed loads and
 // acquires once, ordered before every wave's later loads by the next
 // workgroup barrier.
-template <int DT, int NCMAX, int KMAX>
+template <int DT, int NCMAX, int KMAX, bool FOLD>
 __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   __shared__ int sh_go;
   // dynamic LDS: the selector's running top-N ([R][N] keys, then [R][N] pool
@@ -1094,7 +1264,11 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   extern __shared__ uint64_t s_dyn[];
   if (blockIdx.x < p.G) {
     __shared__ HeadShared<KMAX, kRoundWaves> hsh;
-    stream_block<DT, NCMAX, KMAX>(p, hsh, (u32x4*)((char*)s_dyn + p.lds_tile_offset), sh_go);
+    u32x4* wl = (u32x4*)((char*)s_dyn + p.lds_tile_offset);
+    if constexpr (FOLD)
+      stream_block_fold<DT, NCMAX, KMAX>(p, hsh, wl, sh_go);
+    else
+      stream_block<DT, NCMAX, KMAX>(p, hsh, wl, sh_go);
     return;
   }
 
@@ -1234,6 +1408,24 @@ typedef void (*RoundFn)(Plan);
     default: return KERNEL<DT, NCMAX, 16>;          \
   }
 
+// round kernels: KMAX up to 16 without fold, up to 8 with it
+#define PCTREE_ROUND_KMAX_SWITCH(KERNEL, DT, NCMAX, kmax, FOLD)        \
+  if (FOLD) {                                                         \
+    switch (kmax) {                                                   \
+      case 1: return KERNEL<DT, NCMAX, 1, true>;                      \
+      case 2: return KERNEL<DT, NCMAX, 2, true>;                      \
+      case 4: return KERNEL<DT, NCMAX, 4, true>;                      \
+      default: return KERNEL<DT, NCMAX, 8, true>;                     \
+    }                                                                 \
+  }                                                                   \
+  switch (kmax) {                                                     \
+    case 1: return KERNEL<DT, NCMAX, 1, false>;                       \
+    case 2: return KERNEL<DT, NCMAX, 2, false>;                       \
+    case 4: return KERNEL<DT, NCMAX, 4, false>;                       \
+    case 8: return KERNEL<DT, NCMAX, 8, false>;                       \
+    default: return KERNEL<DT, NCMAX, 16, false>;                     \
+  }
+
 #define PCTREE_DISPATCH(KERNEL, p)                                    \
   if ((p).dtype) {                                                    \
     if ((p).nchunk <= 4) { PCTREE_KMAX_SWITCH(KERNEL, 1, 4, (p).kmax) } \
@@ -1251,7 +1443,20 @@ int nchunk_max(const Plan& p) {
   if (p.dtype) return p.nchunk <= 4 ? 4 : (p.nchunk <= 8 ? 8 : (p.nchunk <= 12 ? 12 : 16));
   return p.nchunk <= 2 ? 2 : 8;
 }
-RoundFn round_fn(const Plan& p) { PCTREE_DISPATCH(round_kernel, p) }
+// The folded form serves rounds whose stages have at most 8 frontier rows.
+bool round_fold(const Plan& p) { return p.R * p.kk <= 8; }
+
+RoundFn round_fn(const Plan& p) {
+  const bool fold = round_fold(p);
+  if (p.dtype) {
+    if (p.nchunk <= 4) { PCTREE_ROUND_KMAX_SWITCH(round_kernel, 1, 4, p.kmax, fold) }
+    if (p.nchunk <= 8) { PCTREE_ROUND_KMAX_SWITCH(round_kernel, 1, 8, p.kmax, fold) }
+    if (p.nchunk <= 12) { PCTREE_ROUND_KMAX_SWITCH(round_kernel, 1, 12, p.kmax, fold) }
+    PCTREE_ROUND_KMAX_SWITCH(round_kernel, 1, 16, p.kmax, fold)
+  }
+  if (p.nchunk <= 2) { PCTREE_ROUND_KMAX_SWITCH(round_kernel, 0, 2, p.kmax, fold) }
+  PCTREE_ROUND_KMAX_SWITCH(round_kernel, 0, 8, p.kmax, fold)
+}
 
 StageFn select_fn(int kmax) {
   switch (kmax) {
