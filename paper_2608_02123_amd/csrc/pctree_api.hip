@@ -110,6 +110,9 @@ void plan_shape(Plan& p, int V, int B, int N, int k, int r, int R, int dtype) {
   p.G = (p.ntiles + p.tiles_per_slice - 1) / p.tiles_per_slice;
   p.maxpool = 1 + p.kk + (B - 1) * p.kk * p.kk;
   p.rows_max = R * p.kk;
+  // the persistent form keeps every stage's partials (blocks read them while
+  // others already publish the next stage); the multi-launch form reuses one
+  p.stages = p.rows_max <= kNarrowRows ? B : 1;
 }
 
 size_t carve_workspace(Plan& p, char* base) {
@@ -130,11 +133,11 @@ size_t carve_workspace(Plan& p, char* base) {
   p.node_score = (float*)take(R * p.maxpool * sizeof(float));
   p.top_key = (uint64_t*)take(R * p.N * sizeof(uint64_t));
   p.top_node = (int*)take(R * p.N * sizeof(int));
-  p.part_key = (uint64_t*)take((size_t)kSlicesMax * p.rows_max * p.kmax * sizeof(uint64_t));
-  p.part_ms = (float2*)take((size_t)kSlicesMax * p.rows_max * sizeof(float2));
+  const size_t parts = (size_t)p.stages * p.rows_max * kSlicesMax;
+  p.part_key = (uint64_t*)take(parts * p.kmax * sizeof(uint64_t));
+  p.part_hd = (SliceHead*)take(parts * sizeof(SliceHead));
   p.req_bad = (int*)take(R * sizeof(int));
-  p.sync = (int*)take((size_t)(p.B + 1) * sizeof(int));
-  p.flags = (int*)take((size_t)kSlicesMax * kFlagStride * sizeof(int));
+  p.tags = (uint64_t*)take((size_t)p.stages * kSlicesMax * sizeof(uint64_t));
   return off;
 }
 

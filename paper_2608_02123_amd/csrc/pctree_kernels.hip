@@ -32,6 +32,9 @@
 #include <math.h>
 
 #include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <random>
 
 #define PCTREE_EMIT_MAX_N 256
 #define PCTREE_MASK_MAX_N 1024
@@ -351,39 +354,48 @@ __device__ __forceinline__ f32x4 mfma_chunk<0>(u32x4 a, u32x4 b, f32x4 acc) {
 // ---------------------------------------------------------------------------
 // prologue: root node, frontier {x_t}, running top-N {root}, head input of x_t
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kEmitThreads) void prologue_kernel(Plan p) {
-  const int req = blockIdx.x;
-  const int tid = threadIdx.x;
+// Per-request outputs and pool entries every form starts from: the root node
+// (token 0 stands in for an invalid root, whose tree is emitted empty), a
+// count of -1 that stays if the round is aborted, the trace's stage-0 row.
+// Threads [tid0, tid0 + nth) of the calling workgroup share the work.
+__device__ void init_request(const Plan& p, int req, int tid, int nth) {
   int root = p.root[req];
   const bool bad = root < 0 || root >= p.V;
   if (bad) root = 0;
-  if (req == 0) {
-    for (int i = tid; i < p.B + 1; i += blockDim.x) p.sync[i] = 0;
-    for (int g = tid; g < p.G; g += blockDim.x) p.flags[(size_t)g * kFlagStride] = 0;
-  }
   if (tid == 0) {
     p.req_bad[req] = bad ? 1 : 0;
-    p.o_count[req] = -1;  // stays -1 if the round is aborted before emission
+    p.o_count[req] = -1;
     const size_t nb = (size_t)req * p.maxpool;
     p.node_tok[nb] = root;
     p.node_par[nb] = -1;
     p.node_depth[nb] = 0;
     p.node_score[nb] = 0.0f;
-    p.top_key[(size_t)req * p.N] = node_key(0.0f, 0, root, 0);
-    p.top_node[(size_t)req * p.N] = 0;
-    p.front_node[req * p.kk] = 0;
-    p.front_tok[req * p.kk] = root;
-    p.front_score[req * p.kk] = 0.0f;
   }
   if (p.t_token) {
     const int n = p.B * p.k;
-    for (int i = tid; i < n; i += blockDim.x) {
+    for (int i = tid; i < n; i += nth) {
       const size_t o = (size_t)req * n + i;
       const bool first = i == 0;
       p.t_token[o] = first ? root : -1;
       p.t_pslot[o] = -1;
       p.t_score[o] = first ? 0.0f : -INFINITY;
     }
+  }
+}
+
+// Multi-launch form: request state in the workspace and the stage-0 head input.
+__global__ __launch_bounds__(kEmitThreads) void prologue_kernel(Plan p) {
+  const int req = blockIdx.x;
+  const int tid = threadIdx.x;
+  init_request(p, req, tid, blockDim.x);
+  int root = p.root[req];
+  if (root < 0 || root >= p.V) root = 0;
+  if (tid == 0) {
+    p.top_key[(size_t)req * p.N] = node_key(0.0f, 0, root, 0);
+    p.top_node[(size_t)req * p.N] = 0;
+    p.front_node[req * p.kk] = 0;
+    p.front_tok[req * p.kk] = root;
+    p.front_score[req * p.kk] = 0.0f;
   }
   for (int j = tid; j < p.r; j += blockDim.x)
     put_activation(p, (size_t)req * p.kk, root, j, p.h[(size_t)req * p.B * p.r + j]);
@@ -546,6 +558,7 @@ __device__ __forceinline__ void tile_step(const Plan& p, const HeadLane& h,
   tile_epilogue<DT, KMAX>(p, h, acc, l, t, h.row_ok, r);
 }
 
+
 // Two tiles on two independent MFMA chains; the second tile's C fragment is
 // moved into columns 8..15 (DPP row_shr:8 onto banks 2-3 of every row), then
 // one epilogue covers both.  t is the lane's own tile (ta or tb by half).
@@ -592,8 +605,9 @@ __device__ __forceinline__ void lds_pair_step(const Plan& p, const HeadLane& h, 
 // Reduce the lanes' row states over the workgroup and publish the slice's
 // partial of every row (best keys and (max, sum)).
 template <int KMAX, int WAVES, bool FOLD = false>
-__device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h, int slice,
-                                                RowAcc<KMAX>& r, HeadShared<KMAX, WAVES>& sh) {
+__device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h, int stage,
+                                                int slice, RowAcc<KMAX>& r,
+                                                HeadShared<KMAX, WAVES>& sh) {
   if constexpr (FOLD) {  // the two lanes of a folded row: col and col ^ 8 (DPP row_ror:8)
     uint64_t o[KMAX];
 #pragma unroll
@@ -632,29 +646,31 @@ __device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h
     if (h.grp == 0 && h.row_ok && h.lead) {
       // write-through (agent-coherent) stores: the arrival count that
       // follows needs no L2 write-back
-      const size_t o = (size_t)h.row * kSlicesMax + slice;
+      const size_t o = ((size_t)stage * p.rows_max + h.row) * kSlicesMax + slice;
       uint64_t* dst = p.part_key + o * KMAX;
 #pragma unroll
       for (int i = 0; i < KMAX; ++i)
         __hip_atomic_store(dst + i, r.list[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      uint64_t* hd = (uint64_t*)(p.part_hd + o);
       const uint64_t ms = ((uint64_t)__float_as_uint(r.s) << 32) | __float_as_uint(r.m);
-      __hip_atomic_store((uint64_t*)(p.part_ms + o), ms, __ATOMIC_RELAXED,
+      __hip_atomic_store(hd, r.list[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(hd + 1, ms, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
 
-// Count this block's arrival at stage d (thread 0; wave 0 wrote the
-// partial).  The partial was stored write-through; waiting for those stores
-// to complete before the relaxed add makes the data reach the coherence point
-// before the count does, without an L2 write-back of the whole cache.
-__device__ __forceinline__ void arrive(const Plan& p, int d) {
+// Announce this slice's stage-d partial (wave 0 stored it write-through):
+// once those stores have completed they are visible at agent scope, and the
+// slice's tag for the stage is set to the call's epoch.  Readers poll the tags.
+__device__ __forceinline__ void publish_tag(const Plan& p, int d, int slice) {
   if (threadIdx.x < 64) {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_waitcnt(0);
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     if (threadIdx.x == 0)
-      __hip_atomic_fetch_add(p.sync + d, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(p.tags + (size_t)d * kSlicesMax + slice, p.epoch, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -709,15 +725,15 @@ __device__ __forceinline__ void head_slice(const Plan& p, int d, int P, int cb, 
       t += WAVES;
     }
   }
-  publish_partial<KMAX, WAVES>(p, h, slice, r, sh);
+  publish_partial<KMAX, WAVES>(p, h, 0, slice, r, sh);
 }
 
-__device__ int wait_flag(const Plan& p, int target);
+__device__ int wait_tags(const Plan& p, int d);
 
 // Tiles a streaming block of the persistent kernel keeps on chip for the
 // whole round: RT per wave in registers and up to LTW per wave in LDS.
 // (64 VGPRs of resident A fragments per lane at most: more spills.)
-__host__ __device__ constexpr int resident_reg_tiles(int ncmax) {
+__host__ __device__ constexpr int resident_reg_tiles(int ncmax, bool fold = false) {
   return ncmax <= 2 ? 4 : (ncmax <= 4 ? 3 : (ncmax <= 8 ? 2 : 1));
 }
 __host__ __device__ constexpr int resident_lds_tiles_per_wave(int ncmax) {
@@ -729,9 +745,139 @@ __host__ __device__ constexpr int resident_lds_tiles_per_wave(int ncmax) {
 // p.lds_tiles to LDS (stored in MFMA fragment order), and only the rest, if
 // any, is streamed at every stage.  Each stage then loads L_d before waiting
 // for the selector's release, reads the new head input and runs the tiles.
+// ---------------------------------------------------------------------------
+// persistent form: replicated selection
+// ---------------------------------------------------------------------------
+// Every workgroup keeps its own copy of the frontier (identical everywhere:
+// all derive it from the same published partials with the same code).
+struct FrontShared {
+  int tok[kNarrowRows];
+  float score[kNarrowRows];
+};
+
+// Head input of the frontier in LDS: [rows][r] at the head's precision, rows
+// padded by 16 bytes so that the 16 columns' B-fragment reads spread over
+// the banks.
+__device__ __forceinline__ int u_stride(const Plan& p) { return p.r * (p.dtype ? 2 : 4) + 16; }
+
+template <int DT>
+__device__ void compute_u(const Plan& p, const FrontShared& fs, int d, int P, char* ul) {
+  constexpr int Q = 4;  // elements per work item
+  const int rows = p.R * P;
+  const int us = u_stride(p);
+  const int n = rows * p.r / Q;
+  for (int base = 0; base < n; base += 2 * (int)blockDim.x) {
+    uint32_t ev[2][Q];
+    f32x4 hv[2];
+    int urow[2], j0[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int e = min(base + q * (int)blockDim.x + (int)threadIdx.x, n - 1) * Q;
+      const int row = e / p.r;
+      const int j = e - row * p.r;
+      const int req = row / P;
+      const int tok = fs.tok[req * p.kk + (row - req * P)];
+      const size_t eo = (size_t)tok * p.r + j;
+      if (DT) {
+        const uint2 v = *(const uint2*)((const uint16_t*)p.E + eo);
+        ev[q][0] = v.x << 16;
+        ev[q][1] = v.x & 0xffff0000u;
+        ev[q][2] = v.y << 16;
+        ev[q][3] = v.y & 0xffff0000u;
+      } else {
+        const u32x4 v = *(const u32x4*)((const float*)p.E + eo);
+#pragma unroll
+        for (int i = 0; i < Q; ++i) ev[q][i] = v[i];
+      }
+      hv[q] = *(const f32x4*)(p.h + ((size_t)req * p.B + d) * p.r + j);
+      urow[q] = row;
+      j0[q] = j;
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      if (base + q * (int)blockDim.x + (int)threadIdx.x < n) {
+        float u[Q];
+#pragma unroll
+        for (int i = 0; i < Q; ++i) u[i] = silu_f32(__uint_as_float(ev[q][i]), hv[q][i]);
+        char* dst = ul + (size_t)urow[q] * us;
+        if (DT) {
+          uint2 v;
+          v.x = (uint32_t)bf16_rne(u[0]) | ((uint32_t)bf16_rne(u[1]) << 16);
+          v.y = (uint32_t)bf16_rne(u[2]) | ((uint32_t)bf16_rne(u[3]) << 16);
+          *(uint2*)(dst + j0[q] * 2) = v;
+        } else {
+          *(f32x4*)(dst + j0[q] * 4) = f32x4{u[0], u[1], u[2], u[3]};
+        }
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// B fragments from the head input in LDS (zero past the rows and the rank).
+template <int DT, int NCMAX>
+__device__ __forceinline__ void load_bfrag_lds(const Plan& p, const HeadLane& h, const char* ul,
+                                               u32x4 (&b)[NCMAX]) {
+  constexpr int KC = DT ? 32 : 16;
+  constexpr int ESZ = DT ? 2 : 4;
+  const char* urow = ul + (size_t)h.col * u_stride(p) + h.grp * (KC / 4) * ESZ;
+#pragma unroll
+  for (int c = 0; c < NCMAX; ++c) {
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (c < p.nchunk && h.b_ok) v = *(const u32x4*)(urow + c * KC * ESZ);
+    b[c] = v;
+  }
+}
+
+
+struct SelShared;
+template <int KMAX>
+__device__ void sel_merge(const Plan& p, int d, int rows, SelShared& sh);
+template <int KMAX>
+__device__ void sel_merge_call(const Plan& p, int d, int rows, SelShared& sh);
+__device__ void sel_frontier(const Plan& p, FrontShared& fs, int d, int P, SelShared& sh);
+
+// Everything a streaming workgroup does before its stage-d stream: wait for
+// stage d-1 to be complete, derive the stage-d frontier from its partials,
+// and build the head input in LDS.  Returns false if the round was aborted.
+template <int DT, int KMAX, bool CALL>
+__device__ __forceinline__ bool stage_inputs(const Plan& p, int d, FrontShared& fs,
+                                             SelShared& ssh, char* ul, int& sh_go) {
+  if (d > 0) {
+    if (threadIdx.x < 64) {
+      const int ok = wait_tags(p, d - 1);
+      if (threadIdx.x == 0) sh_go = ok;
+    }
+    __syncthreads();
+    if (!sh_go) return false;
+    const int pp = d == 1 ? 1 : p.kk;
+    if constexpr (CALL)
+      sel_merge_call<KMAX>(p, d - 1, p.R * pp, ssh);
+    else
+      sel_merge<KMAX>(p, d - 1, p.R * pp, ssh);
+    sel_frontier(p, fs, d - 1, pp, ssh);
+  }
+  compute_u<DT>(p, fs, d, d == 0 ? 1 : p.kk, ul);
+  return true;
+}
+
+// The stage-0 frontier: each request's root (token 0 stands in for an invalid
+// one, whose tree is emitted empty).
+__device__ __forceinline__ void init_front(const Plan& p, FrontShared& fs) {
+  for (int req = threadIdx.x; req < p.R; req += blockDim.x) {
+    const int root = p.root[req];
+    fs.tok[req * p.kk] = root < 0 || root >= p.V ? 0 : root;
+    fs.score[req * p.kk] = 0.0f;
+  }
+}
+
+// One streaming workgroup of the persistent round: a fixed V-slice whose W
+// tiles stay on chip (RT per wave in registers, up to LTW per wave in LDS in
+// fragment order, the rest re-read every stage), B stages of frontier
+// selection + head stream + partial publication.
 template <int DT, int NCMAX, int KMAX>
-__device__ void stream_block(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, u32x4* wl,
-                             int& sh_go) {
+__device__ void stream_block(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, SelShared& ssh,
+                             FrontShared& fs, char* ul, u32x4* wl, int& sh_go) {
   constexpr int WAVES = kRoundWaves;
   constexpr int RT = resident_reg_tiles(NCMAX);
   constexpr int LTW = resident_lds_tiles_per_wave(NCMAX);
@@ -745,6 +891,7 @@ __device__ void stream_block(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, u
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
 
+  init_front(p, fs);
   {  // load the resident tiles (the lane geometry of A does not depend on rows)
     const HeadLane h0(p, 1, 0);
     u32x4 a[NCMAX];
@@ -772,13 +919,9 @@ __device__ void stream_block(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, u
 #pragma unroll
     for (int q = 0; q < LTW; ++q)
       load_lfrag<DT>(p, h, d, min(lds0 + wave + WAVES * q, t1 - 1), llds[q]);
-    if (d > 0) {
-      if (threadIdx.x == 0) sh_go = wait_flag(p, d);
-      __syncthreads();
-      if (!sh_go) return;
-    }
+    if (!stage_inputs<DT, KMAX, true>(p, d, fs, ssh, ul, sh_go)) return;
     u32x4 bfrag[NCMAX];
-    load_bfrag<DT, NCMAX>(p, h, bfrag);
+    load_bfrag_lds<DT, NCMAX>(p, h, ul, bfrag);
     RowAcc<KMAX> r;
     r.init();
 #pragma unroll
@@ -802,8 +945,8 @@ __device__ void stream_block(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, u
       load_lfrag<DT>(p, h, d, t, T.l);
       tile_step<DT, NCMAX, KMAX>(p, h, T.a, bfrag, T.l, t, r);
     }
-    publish_partial<KMAX, WAVES>(p, h, slice, r, sh);
-    arrive(p, d);
+    publish_partial<KMAX, WAVES>(p, h, d, slice, r, sh);
+    publish_tag(p, d, slice);
   }
 }
 
@@ -811,10 +954,11 @@ __device__ void stream_block(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, u
 // pairs whose C fragments are folded into one set of 16 columns (see
 // HeadLane), so every lane's epilogue works on a live row.
 template <int DT, int NCMAX, int KMAX>
-__device__ void stream_block_fold(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, u32x4* wl,
+__device__ void stream_block_fold(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh,
+                                  SelShared& ssh, FrontShared& fs, char* ul, u32x4* wl,
                                   int& sh_go) {
   constexpr int WAVES = kRoundWaves;
-  constexpr int RT = resident_reg_tiles(NCMAX);
+  constexpr int RT = resident_reg_tiles(NCMAX, true);
   constexpr int LTW = resident_lds_tiles_per_wave(NCMAX);
   constexpr int RP = (RT + 1) / 2;   // register-resident pairs per wave
   constexpr int LP = (LTW + 1) / 2;  // LDS-resident pairs per wave
@@ -828,6 +972,7 @@ __device__ void stream_block_fold(const Plan& p, HeadShared<KMAX, kRoundWaves>& 
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
 
+  init_front(p, fs);
   {
     const HeadLane h0(p, 1, 0);
     u32x4 a[NCMAX];
@@ -856,13 +1001,9 @@ __device__ void stream_block_fold(const Plan& p, HeadShared<KMAX, kRoundWaves>& 
 #pragma unroll
     for (int q = 0; q < LP; ++q)
       load_lfrag<DT>(p, h, d, min(lds0 + wave + WAVES * (2 * q + h.half), t1 - 1), llds[q]);
-    if (d > 0) {
-      if (threadIdx.x == 0) sh_go = wait_flag(p, d);
-      __syncthreads();
-      if (!sh_go) return;
-    }
+    if (!stage_inputs<DT, KMAX, false>(p, d, fs, ssh, ul, sh_go)) return;
     u32x4 bfrag[NCMAX];
-    load_bfrag<DT, NCMAX>(p, h, bfrag);
+    load_bfrag_lds<DT, NCMAX>(p, h, ul, bfrag);
     RowAcc<KMAX> r;
     r.init();
 #pragma unroll
@@ -898,8 +1039,8 @@ __device__ void stream_block_fold(const Plan& p, HeadShared<KMAX, kRoundWaves>& 
       load_lfrag<DT>(p, h, d, tl, l);
       tile_pair_step<DT, NCMAX, KMAX>(p, h, a0, a1, bfrag, l, tl, h.half ? okb : true, r);
     }
-    publish_partial<KMAX, WAVES, true>(p, h, slice, r, sh);
-    arrive(p, d);
+    publish_partial<KMAX, WAVES, true>(p, h, d, slice, r, sh);
+    publish_tag(p, d, slice);
   }
 }
 
@@ -938,7 +1079,7 @@ struct SelShared {
 // into the running global top-N (Sec. 4.2) and write the next head input.
 // Needs blockDim >= 512 and nreq * P * k' <= 256.
 __device__ void stage_select(const Plan& p, const State& st, int d, int P, int req0, int nreq,
-                             SelShared& sh) {
+                             SelShared& sh, bool act) {
   const int tid = threadIdx.x;
   const int kk = p.kk;
   const int per_req = P * kk;
@@ -1022,64 +1163,148 @@ __device__ void stage_select(const Plan& p, const State& st, int d, int P, int r
     }
   }
   __syncthreads();
-  if (more) write_activations(p, st, d + 1, req0, nreq);
+  if (more && act) write_activations(p, st, d + 1, req0, nreq);
 }
 
-// Merge the slice partials of the R*P rows (<= 16) of a stage into each row's
-// lse and top-k' children, one wave per row.  Every lane loads the complete
-// lists of its slices in one batch (one memory round trip), merges them into
-// one sorted list, and k' rounds of a wave-wide maximum pop the row's best
-// keys (the lane holding the winner shifts its list).
-template <int KMAX, int WAVES>
-__device__ void merge_narrow(const Plan& p, int rows, SelShared& sh) {
-  constexpr int CH = KMAX >= 16 ? 2 : (KMAX >= 8 ? 4 : 8);  // slices per lane per batch
+// The top-k' children and the lse of each of the R*P (<= 16) rows of stage d
+// from the published slice partials, one wave per row.  A row's top-k' lie
+// in the k' slices with the largest best keys (any other slice is beaten k'
+// times over), so the heads of all slices are read first (with the (max,
+// sum) pairs), then the lists of those k' slices only.  Keys are unique
+// (the token is part of them), so each pop of a wave-wide maximum removes
+// exactly one entry.
+template <int KMAX, int HPL>
+__device__ __forceinline__ void sel_merge_rows(const Plan& p, int d, int rows, SelShared& sh) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int kk = p.kk;
+  const int nwave = blockDim.x >> 6;
   const int G = p.G;
-  for (int row = wave; row < rows; row += WAVES) {
+  const int kk = p.kk;
+  const int nwin = min(kk, G);
+  for (int row = wave; row < rows; row += nwave) {
+    const size_t base = ((size_t)d * p.rows_max + row) * kSlicesMax;
+    uint64_t hk[HPL];
+    float hm[HPL], hs[HPL];
+#pragma unroll
+    for (int c = 0; c < HPL; ++c) {
+      const SliceHead v = p.part_hd[base + min(lane + 64 * c, G - 1)];
+      hk[c] = v.key;
+      hm[c] = v.m;
+      hs[c] = v.s;
+    }
     float m = kNegBig, s = 0.0f;
-    uint64_t acc[KMAX];
 #pragma unroll
-    for (int i = 0; i < KMAX; ++i) acc[i] = 0;
-    const uint64_t* keys = p.part_key + (size_t)row * kSlicesMax * KMAX;
-    const float2* mss = p.part_ms + (size_t)row * kSlicesMax;
-    for (int base = 0; base < G; base += 64 * CH) {
-      uint64_t lst[CH][KMAX];
-      float2 ms[CH];
+    for (int c = 0; c < HPL; ++c) {
+      if (lane + 64 * c < G)
+        lse_combine(m, s, hm[c], hs[c]);
+      else
+        hk[c] = 0;
+    }
+    // the lane's heads sorted (descending), then k' pops of the wave maximum
 #pragma unroll
-      for (int c = 0; c < CH; ++c) {
-        const int g = min(base + lane + 64 * c, G - 1);
+    for (int c = 1; c < HPL; ++c) {
 #pragma unroll
-        for (int i = 0; i < KMAX; ++i) lst[c][i] = keys[(size_t)g * KMAX + i];
-        ms[c] = mss[g];
-      }
-#pragma unroll
-      for (int c = 0; c < CH; ++c) {
-        if (base + lane + 64 * c < G) {
-          list_merge(acc, lst[c]);
-          lse_combine(m, s, ms[c].x, ms[c].y);
-        }
+      for (int i = c; i > 0; --i) {
+        const uint64_t a = hk[i - 1], b = hk[i];
+        const bool sw = b > a;
+        hk[i - 1] = sw ? b : a;
+        hk[i] = sw ? a : b;
       }
     }
-    {  // row lse: the wave's max, then the sum rescaled to it
-      const float M = wave_max_f32(m);
-      s = wave_sum_f32(s * exp2f((m - M) * kLog2e));
-      m = M;
+    const float M = wave_max_f32(m);
+    const float S = wave_sum_f32(s * exp2f((m - M) * kLog2e));
+    uint64_t won = 0;  // lane i keeps the i-th largest head
+#pragma unroll
+    for (int it = 0; it < KMAX; ++it) {
+      if (it < nwin) {
+        const uint64_t best = wave_max_u64(hk[0]);
+        if (hk[0] == best) {
+#pragma unroll
+          for (int c = 0; c + 1 < HPL; ++c) hk[c] = hk[c + 1];
+          hk[HPL - 1] = 0;
+        }
+        if (lane == it) won = best;
+      }
+    }
+    const int myslice = lane < nwin ? min(child_key_token(won) / (p.tiles_per_slice * kTile), G - 1) : 0;
+    uint64_t lst[KMAX];
+    {
+      const uint64_t* src = p.part_key + (base + myslice) * KMAX;
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) lst[i] = src[i];
+      if (lane >= nwin) {
+#pragma unroll
+        for (int i = 0; i < KMAX; ++i) lst[i] = 0;
+      }
     }
 #pragma unroll
     for (int it = 0; it < KMAX; ++it) {
       if (it < kk) {
-        const uint64_t best = wave_max_u64(acc[0]);
-        if (acc[0] == best) {
+        const uint64_t best = wave_max_u64(lst[0]);
+        if (lst[0] == best) {
 #pragma unroll
-          for (int i = 0; i + 1 < KMAX; ++i) acc[i] = acc[i + 1];
-          acc[KMAX - 1] = 0;
+          for (int i = 0; i + 1 < KMAX; ++i) lst[i] = lst[i + 1];
+          lst[KMAX - 1] = 0;
         }
         if (lane == 0) sh.rowkeys[row][it] = best;
       }
     }
-    if (lane == 0) sh.lse[row] = m + logf(s);
+    if (lane == 0) sh.lse[row] = M + logf(S);
+  }
+  __syncthreads();
+}
+
+// The persistent form uses at most kRoundSlicesMax slices (one per CU).
+template <int KMAX>
+__device__ __forceinline__ void sel_merge(const Plan& p, int d, int rows, SelShared& sh) {
+  if (p.G <= 64)
+    sel_merge_rows<KMAX, 1>(p, d, rows, sh);
+  else if (p.G <= 128)
+    sel_merge_rows<KMAX, 2>(p, d, rows, sh);
+  else
+    sel_merge_rows<KMAX, kRoundSlicesMax / 64>(p, d, rows, sh);
+}
+
+// Out-of-line form for callers whose own registers are short (the unfolded
+// streaming loop): the merge's registers do not count against theirs, at the
+// price of reading the plan through memory.
+template <int KMAX>
+__device__ __noinline__ void sel_merge_call(const Plan& p, int d, int rows, SelShared& sh) {
+  sel_merge<KMAX>(p, d, rows, sh);
+}
+
+// The frontier of stage d + 1 from the stage-d rows in sh (a streaming
+// workgroup's share of stage_select: scores, ranks within each request's
+// layer, the k' best become the new slots).
+__device__ void sel_frontier(const Plan& p, FrontShared& fs, int d, int P, SelShared& sh) {
+  const int tid = threadIdx.x;
+  const int kk = p.kk;
+  const int per_req = P * kk;
+  const int ncand = p.R * per_req;
+  int tok = 0;
+  float score = 0.0f;
+  if (tid < ncand) {
+    const int rq = tid / per_req;
+    const int ci = tid - rq * per_req;
+    const int pr = ci / kk;
+    const int j = ci - pr * kk;
+    const int lrow = rq * P + pr;
+    const uint64_t ck = sh.rowkeys[lrow][j];
+    tok = min(max(child_key_token(ck), 0), p.V - 1);
+    score = fs.score[rq * kk + pr] + (child_key_value(ck) - sh.lse[lrow]);
+    sh.ckey[tid] = node_key(score, d + 1, tok, pr);
+  }
+  __syncthreads();
+  int rank = kk;
+  if (tid < ncand) {
+    const int rq = tid / per_req;
+    rank = count_greater(sh.ckey + rq * per_req, per_req, sh.ckey[tid]);
+  }
+  __syncthreads();  // every frontier slot was read above
+  if (tid < ncand && rank < kk) {
+    const int rq = tid / per_req;
+    fs.tok[rq * kk + rank] = tok;
+    fs.score[rq * kk + rank] = score;
   }
   __syncthreads();
 }
@@ -1202,85 +1427,76 @@ __device__ void emit_request(const Plan& p, const State& st, int req) {
   __syncthreads();
 }
 
-// ---------------------------------------------------------------------------
-// narrow form: one persistent cooperative kernel per round
-// ---------------------------------------------------------------------------
-// Thread 0 of workgroup g waits until its own flag line flags[g * 64] reaches
-// `target` (one line per workgroup: a single word polled by every workgroup
-// would queue all polls at one memory channel).  It polls with relaxed loads
-// (an acquire load would invalidate the L2 on every poll) and acquires once at
-// the end.  Every wait is bounded by p.spin_ticks of the device wall clock; on
-// a timeout the workgroup raises the abort word and leaves the round, which
-// then ends without emission (count stays -1).
-__device__ int wait_flag(const Plan& p, int target) {
-  int* flag = p.flags + (size_t)blockIdx.x * kFlagStride;
+// Wave 0 waits until every slice's stage-d tag holds this call's epoch, then
+// acquires (the partials were stored write-through before the tags).  Polls
+// use relaxed agent-scope loads (an acquire per poll would invalidate the L2
+// each time).  Bounded by p.spin_ticks of the device wall clock: returns 0 on
+// a timeout and the workgroup leaves the round, which then ends without
+// emission (count stays -1).
+__device__ int wait_tags(const Plan& p, int d) {
+  constexpr int TPL = kRoundSlicesMax / 64;
+  const int lane = threadIdx.x & 63;
+  const uint64_t* tg = p.tags + (size_t)d * kSlicesMax;
   const long long t0 = wall_clock64();
   for (;;) {
-    if (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target) {
+    uint64_t v[TPL];
+#pragma unroll
+    for (int c = 0; c < TPL; ++c)
+      v[c] = __hip_atomic_load(tg + min(lane + 64 * c, p.G - 1), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+    bool ok = true;
+#pragma unroll
+    for (int c = 0; c < TPL; ++c) ok = ok && v[c] == p.epoch;
+    if (__all(ok)) {
       __atomic_thread_fence_agent_acquire();
       return 1;
     }
-    if (wall_clock64() - t0 > p.spin_ticks) {
-      __hip_atomic_store(p.sync + p.B, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return 0;
-    }
-    __builtin_amdgcn_s_sleep(2);
-  }
-}
-
-// Wait (thread 0) until the arrival counter of stage d has counted every
-// streaming workgroup, then acquire their partials.  Bounded like wait_flag.
-__device__ int wait_arrivals(const Plan& p, int d) {
-  int* cnt = p.sync + d;
-  const long long t0 = wall_clock64();
-  for (;;) {
-    if (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= p.G) {
-      __atomic_thread_fence_agent_acquire();
-      return 1;
-    }
-    if (wall_clock64() - t0 > p.spin_ticks) {
-      __hip_atomic_store(p.sync + p.B, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return 0;
-    }
+    if (wall_clock64() - t0 > p.spin_ticks) return 0;
     __builtin_amdgcn_s_sleep(1);
   }
 }
 
-// Blocks [0, G) stream one V-slice each per stage; block G is the selector:
-// it keeps the frontier and the running top-N in LDS for the whole round,
-// waits for the G partials of a stage, merges and selects, writes the next
-// head input and raises every streaming block's flag; after the last stage it
-// emits the tree.  Slice partials are stored write-through at agent scope and
-// a streaming block waits for those stores to complete before it counts its
-// arrival; the selector publishes the head inputs with an agent-scope release
-// before the flags.  A consumer's thread 0 polls with relaxed loads and
-// acquires once, ordered before every wave's later loads by the next
-// workgroup barrier.
+
+// Blocks [0, G) stream one V-slice each; block G is the keeper.  Before
+// stage d every block waits for stage d-1 to be complete (its flag line,
+// raised by the workgroup that completes the arrival count) and derives the
+// stage-d frontier from the published partials itself, so no head input
+// travels between workgroups.  The keeper makes the same selection and in
+// addition keeps the pool, the trace and the running top-N (in LDS), and
+// emits the tree after the last stage.  Slice partials are stored
+// write-through at agent scope and a block waits for those stores to complete
+// before it counts its arrival; a waiting block's thread 0 polls with relaxed
+// loads and acquires once, ordered before every wave's later loads by the
+// next workgroup barrier.
 template <int DT, int NCMAX, int KMAX, bool FOLD>
 __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   __shared__ int sh_go;
-  // dynamic LDS: the selector's running top-N ([R][N] keys, then [R][N] pool
-  // ids); the streaming blocks' resident W tiles from p.lds_tile_offset
+  __shared__ SelShared ssh;
+  // dynamic LDS: the head input of the frontier (streaming blocks), the
+  // keeper's running top-N, the streaming blocks' resident W tiles
   extern __shared__ uint64_t s_dyn[];
+  char* dyn = (char*)s_dyn;
   if (blockIdx.x < p.G) {
     __shared__ HeadShared<KMAX, kRoundWaves> hsh;
-    u32x4* wl = (u32x4*)((char*)s_dyn + p.lds_tile_offset);
+    __shared__ FrontShared fs;
+    u32x4* wl = (u32x4*)(dyn + p.lds_tile_offset);
     if constexpr (FOLD)
-      stream_block_fold<DT, NCMAX, KMAX>(p, hsh, wl, sh_go);
+      stream_block_fold<DT, NCMAX, KMAX>(p, hsh, ssh, fs, dyn, wl, sh_go);
     else
-      stream_block<DT, NCMAX, KMAX>(p, hsh, wl, sh_go);
+      stream_block<DT, NCMAX, KMAX>(p, hsh, ssh, fs, dyn, wl, sh_go);
     return;
   }
 
-  // the selector block
-  __shared__ SelShared ssh;
+  // the keeper
   __shared__ int s_front_node[kNarrowRows], s_front_tok[kNarrowRows];
   __shared__ float s_front_score[kNarrowRows];
-  uint64_t* s_top = s_dyn;
+  uint64_t* s_top = (uint64_t*)(dyn + p.lds_top_offset);
   const State st{s_front_node, s_front_tok, s_front_score, s_top,
                  (int*)(s_top + (size_t)p.R * p.N)};
+  for (int req = 0; req < p.R; ++req) init_request(p, req, threadIdx.x, blockDim.x);
   for (int req = threadIdx.x; req < p.R; req += blockDim.x) {
-    const int root = p.req_bad[req] ? 0 : p.root[req];
+    const int r0 = p.root[req];
+    const int root = r0 < 0 || r0 >= p.V ? 0 : r0;
     st.front_node[req * p.kk] = 0;
     st.front_tok[req * p.kk] = root;
     st.front_score[req * p.kk] = 0.0f;
@@ -1289,21 +1505,16 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   }
   for (int d = 0; d < p.B; ++d) {
     const int P = d == 0 ? 1 : p.kk;
-    if (threadIdx.x == 0) sh_go = wait_arrivals(p, d);
+    if (threadIdx.x < 64) {
+      const int ok = wait_tags(p, d);
+      if (threadIdx.x == 0) sh_go = ok;
+    }
     __syncthreads();
     if (!sh_go) return;
-    merge_narrow<KMAX, kRoundWaves>(p, p.R * P, ssh);
-    stage_select(p, st, d, P, 0, p.R, ssh);
-    if (d + 1 < p.B) {
-      __syncthreads();
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-      for (int g = threadIdx.x; g < p.G; g += blockDim.x)
-        __hip_atomic_store(p.flags + (size_t)g * kFlagStride, d + 1, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-    } else {
-      for (int req = 0; req < p.R; ++req) emit_request(p, st, req);
-    }
+    sel_merge<KMAX>(p, d, p.R * P, ssh);
+    stage_select(p, st, d, P, 0, p.R, ssh, false);
   }
+  for (int req = 0; req < p.R; ++req) emit_request(p, st, req);
 }
 
 // ---------------------------------------------------------------------------
@@ -1342,8 +1553,8 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, i
 #pragma unroll
       for (int i = 0; i < KMAX; ++i) other[i] = p.part_key[o * KMAX + i];
       list_merge(list, other);
-      const float2 ms = p.part_ms[o];
-      lse_combine(m, s, ms.x, ms.y);
+      const SliceHead hd = p.part_hd[o];
+      lse_combine(m, s, hd.m, hd.s);
     }
   }
 #pragma unroll
@@ -1374,7 +1585,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, i
     }
   }
   __syncthreads();
-  stage_select(p, global_state(p), d, P, req, 1, ssh);
+  stage_select(p, global_state(p), d, P, req, 1, ssh, true);
 }
 
 __global__ __launch_bounds__(kEmitThreads) void emit_kernel(Plan p) {
@@ -1468,6 +1679,26 @@ StageFn select_fn(int kmax) {
   }
 }
 
+// Call tags of the persistent form: a 64-bit sequence started at a random
+// point, skipping 0 and all ones (fill patterns).  Stale tags in a reused
+// workspace come from other calls, so they never equal the current one; a
+// workspace that was never used by this process matches only by chance
+// (2^-64 per word).
+uint64_t next_epoch() {
+  static std::atomic<uint64_t> seq{[] {
+    std::random_device rd;
+    uint64_t x = ((uint64_t)rd() << 32) ^ rd() ^
+                 (uint64_t)std::chrono::high_resolution_clock::now().time_since_epoch().count();
+    x = (x ^ (x >> 30)) * 0xbf58476d1ce4e5b9ull;  // SplitMix64 output mix
+    x = (x ^ (x >> 27)) * 0x94d049bb133111ebull;
+    return x ^ (x >> 31);
+  }()};
+  for (;;) {
+    const uint64_t e = seq.fetch_add(1, std::memory_order_relaxed);
+    if (e != 0 && e != ~0ull) return e;
+  }
+}
+
 // Per-device facts for the persistent launch, queried once per device.
 struct DeviceInfo {
   int cus = 0;
@@ -1504,12 +1735,16 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
     rfn = round_fn(p);
     // one streaming slice per remaining CU (at most kSlicesMax) plus the
     // selector block: every workgroup is resident at once
-    const int target = std::max(1, std::min(di.cus - 1, kSlicesMax));
+    const int target = std::max(1, std::min(di.cus - 1, kRoundSlicesMax));
     p.tiles_per_slice = (p.ntiles + target - 1) / target;
     p.G = (p.ntiles + p.tiles_per_slice - 1) / p.tiles_per_slice;
-    // dynamic LDS: the selector's top-N, then as many resident W tiles as fit
+    // dynamic LDS: the frontier's head input, the keeper's top-N, then as
+    // many resident W tiles as fit
     const int ncmax = nchunk_max(p);
-    const size_t top = ((size_t)p.R * p.N * (sizeof(uint64_t) + sizeof(int)) + 255) & ~(size_t)255;
+    const size_t ubytes =
+        ((size_t)p.rows_max * (p.r * (p.dtype ? 2 : 4) + 16) + 255) & ~(size_t)255;
+    const size_t top = ubytes + (((size_t)p.R * p.N * (sizeof(uint64_t) + sizeof(int)) + 255) &
+                                 ~(size_t)255);
     const size_t tile_bytes = (size_t)ncmax * 64 * 16;
     hipFuncAttributes attr{};
     int lds_max = 0;
@@ -1519,10 +1754,12 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
             hipSuccess &&
         hipFuncGetAttributes(&attr, (const void*)rfn) == hipSuccess) {
       const long room = (long)lds_max - (long)attr.sharedSizeBytes - (long)top - 1024;
-      const int want = std::max(0, p.tiles_per_slice - resident_reg_tiles(ncmax) * kRoundWaves);
+      const int want =
+          std::max(0, p.tiles_per_slice - resident_reg_tiles(ncmax, round_fold(p)) * kRoundWaves);
       const int cap = resident_lds_tiles_per_wave(ncmax) * kRoundWaves;
       p.lds_tiles = room > 0 ? (int)std::min<long>({room / (long)tile_bytes, (long)want, (long)cap})
                              : 0;
+      p.lds_top_offset = (int)ubytes;
       p.lds_tile_offset = (int)top;
       smem = top + (size_t)p.lds_tiles * tile_bytes;
       if (hipFuncSetAttribute((const void*)rfn, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -1534,7 +1771,7 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
   }
   if (narrow && fit > 0) {
     p.spin_ticks = 2 * di.ticks_per_s;  // a stage never legitimately waits 2 s
-    hipLaunchKernelGGL(prologue_kernel, dim3(p.R), dim3(kEmitThreads), 0, st, p);
+    p.epoch = next_epoch();
     void* args[] = {&p};
     const bool prof = profile_on();
     if (prof) profile_mark(st, "round_kernel");

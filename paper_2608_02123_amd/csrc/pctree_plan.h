@@ -10,6 +10,7 @@ namespace pctree {
 
 constexpr int kTile = 16;           // tokens per MFMA output tile (M of 16x16xK)
 constexpr int kSlicesMax = 512;     // V-slices of one head launch
+constexpr int kRoundSlicesMax = 256;  // V-slices of the persistent round kernel
 constexpr int kHeadThreads = 256;   // 4 waves
 constexpr int kSelectThreads = 1024;
 constexpr int kEmitThreads = 256;
@@ -17,6 +18,13 @@ constexpr int kMaskThreads = 256;
 constexpr int kRoundWaves = 8;       // waves per WG of the persistent round kernel
 constexpr int kNarrowRows = 16;      // frontier rows (R * k') one column block holds
 constexpr int kFlagStride = 64;      // ints between two workgroups' flag words (256 B)
+
+// What a streaming workgroup publishes per (stage, row, slice) besides its
+// candidate list: the list's best key and the slice's (row max, sum of exp).
+struct SliceHead {
+  uint64_t key;
+  float m, s;
+};
 
 // Everything one round needs, passed by value to every kernel.
 struct Plan {
@@ -27,6 +35,7 @@ struct Plan {
   int G, tiles_per_slice, ntiles;   // head-stream V-slicing
   int maxpool;                      // 1 + kk + (B-1) kk^2
   int rows_max;                     // R * kk
+  int stages;                       // stages with their own partial buffers (B, or 1)
 
   // inputs
   const void* L;
@@ -59,15 +68,15 @@ struct Plan {
   float* node_score; // [R][maxpool]
   uint64_t* top_key; // [R][N] running global top-N (sorted, descending)
   int* top_node;     // [R][N]
-  uint64_t* part_key;// [rows_max][kSlicesMax][kmax] per-slice candidate lists
-  float2* part_ms;   // [rows_max][kSlicesMax] per-slice (row max, sum of exp)
+  uint64_t* part_key;// [stages][rows_max][kSlicesMax][kmax] per-slice candidate lists
+  SliceHead* part_hd;// [stages][rows_max][kSlicesMax] per-slice best key, (max, sum)
   int* req_bad;      // [R] root token outside [0, V)
-  int* sync;         // [B + 1]: per-depth arrival counters, then the abort word of
-                     // the persistent round kernel
-  int* flags;        // [kSlicesMax * kFlagStride]: per-workgroup "stage ready" lines
+  uint64_t* tags;    // [stages][kSlicesMax]: call tag of each published slice partial
+  uint64_t epoch;    // this call's tag (unique per call; never 0 or all ones)
   long long spin_ticks;  // device wall-clock ticks a wait may last before aborting
   int lds_tiles;         // W tiles a streaming block keeps in LDS for the whole round
-  int lds_tile_offset;   // byte offset of those tiles in the dynamic LDS
+  int lds_top_offset;    // byte offset of the keeper's running top-N in the dynamic LDS
+  int lds_tile_offset;   // byte offset of the resident W tiles in the dynamic LDS
 };
 
 // Workspace layout for a plan; offsets are 256-byte aligned.  With base ==
