@@ -1775,8 +1775,13 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
     void* args[] = {&p};
     const bool prof = profile_on();
     if (prof) profile_mark(st, "round_kernel");
-    const hipError_t e = hipLaunchCooperativeKernel((const void*)rfn, dim3(p.G + 1),
-                                                    dim3(kRoundWaves * 64), args, smem, st);
+    // An ordinary launch: the G + 1 workgroups (at most one per CU, checked
+    // above) are all resident on an otherwise idle device.  A cooperative
+    // launch would guarantee it even beside other work, but costs ~18 us of
+    // dispatch per call here; with other kernels on the device a workgroup
+    // may start late, which the bounded waits absorb (or the round aborts).
+    const hipError_t e = hipLaunchKernel((const void*)rfn, dim3(p.G + 1),
+                                         dim3(kRoundWaves * 64), args, smem, st);
     if (prof) profile_mark(st, "round_kernel");
     if (e != hipSuccess) return e;
     return hipGetLastError();
