@@ -734,6 +734,7 @@ __device__ int wait_tags(const Plan& p, int d);
 // whole round: RT per wave in registers and up to LTW per wave in LDS.
 // (64 VGPRs of resident A fragments per lane at most: more spills.)
 __host__ __device__ constexpr int resident_reg_tiles(int ncmax, bool fold = false) {
+  if (fold) return ncmax <= 2 ? 4 : (ncmax <= 4 ? 3 : (ncmax <= 8 ? 3 : 1));
   return ncmax <= 2 ? 4 : (ncmax <= 4 ? 3 : (ncmax <= 8 ? 2 : 1));
 }
 __host__ __device__ constexpr int resident_lds_tiles_per_wave(int ncmax) {
@@ -833,16 +834,29 @@ __device__ __forceinline__ void load_bfrag_lds(const Plan& p, const HeadLane& h,
 struct SelShared;
 template <int KMAX>
 __device__ void sel_merge(const Plan& p, int d, int rows, SelShared& sh);
-template <int KMAX>
-__device__ void sel_merge_call(const Plan& p, int d, int rows, SelShared& sh);
 __device__ void sel_frontier(const Plan& p, FrontShared& fs, int d, int P, SelShared& sh);
+
+// The frontier of stage d from the stage-(d-1) partials and its head input in
+// LDS.  Out of line, with the plan read from an LDS copy: its registers do
+// not count against the W tiles the streaming loop keeps resident.
+template <int DT, int KMAX>
+__device__ __noinline__ void next_inputs(const Plan& p, int d, FrontShared& fs, SelShared& ssh,
+                                         char* ul) {
+  if (d > 0) {
+    const int pp = d == 1 ? 1 : p.kk;
+    sel_merge<KMAX>(p, d - 1, p.R * pp, ssh);
+    sel_frontier(p, fs, d - 1, pp, ssh);
+  }
+  compute_u<DT>(p, fs, d, d == 0 ? 1 : p.kk, ul);
+}
 
 // Everything a streaming workgroup does before its stage-d stream: wait for
 // stage d-1 to be complete, derive the stage-d frontier from its partials,
 // and build the head input in LDS.  Returns false if the round was aborted.
-template <int DT, int KMAX, bool CALL>
-__device__ __forceinline__ bool stage_inputs(const Plan& p, int d, FrontShared& fs,
-                                             SelShared& ssh, char* ul, int& sh_go) {
+template <int DT, int KMAX>
+__device__ __forceinline__ bool stage_inputs(const Plan& p, const Plan& sp, int d,
+                                             FrontShared& fs, SelShared& ssh, char* ul,
+                                             int& sh_go) {
   if (d > 0) {
     if (threadIdx.x < 64) {
       const int ok = wait_tags(p, d - 1);
@@ -850,14 +864,8 @@ __device__ __forceinline__ bool stage_inputs(const Plan& p, int d, FrontShared& 
     }
     __syncthreads();
     if (!sh_go) return false;
-    const int pp = d == 1 ? 1 : p.kk;
-    if constexpr (CALL)
-      sel_merge_call<KMAX>(p, d - 1, p.R * pp, ssh);
-    else
-      sel_merge<KMAX>(p, d - 1, p.R * pp, ssh);
-    sel_frontier(p, fs, d - 1, pp, ssh);
   }
-  compute_u<DT>(p, fs, d, d == 0 ? 1 : p.kk, ul);
+  next_inputs<DT, KMAX>(sp, d, fs, ssh, ul);
   return true;
 }
 
@@ -876,8 +884,8 @@ __device__ __forceinline__ void init_front(const Plan& p, FrontShared& fs) {
 // fragment order, the rest re-read every stage), B stages of frontier
 // selection + head stream + partial publication.
 template <int DT, int NCMAX, int KMAX>
-__device__ void stream_block(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, SelShared& ssh,
-                             FrontShared& fs, char* ul, u32x4* wl, int& sh_go) {
+__device__ void stream_block(const Plan& p, const Plan& sp, HeadShared<KMAX, kRoundWaves>& sh,
+                             SelShared& ssh, FrontShared& fs, char* ul, u32x4* wl, int& sh_go) {
   constexpr int WAVES = kRoundWaves;
   constexpr int RT = resident_reg_tiles(NCMAX);
   constexpr int LTW = resident_lds_tiles_per_wave(NCMAX);
@@ -919,7 +927,7 @@ __device__ void stream_block(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, S
 #pragma unroll
     for (int q = 0; q < LTW; ++q)
       load_lfrag<DT>(p, h, d, min(lds0 + wave + WAVES * q, t1 - 1), llds[q]);
-    if (!stage_inputs<DT, KMAX, true>(p, d, fs, ssh, ul, sh_go)) return;
+    if (!stage_inputs<DT, KMAX>(p, sp, d, fs, ssh, ul, sh_go)) return;
     u32x4 bfrag[NCMAX];
     load_bfrag_lds<DT, NCMAX>(p, h, ul, bfrag);
     RowAcc<KMAX> r;
@@ -954,9 +962,9 @@ __device__ void stream_block(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh, S
 // pairs whose C fragments are folded into one set of 16 columns (see
 // HeadLane), so every lane's epilogue works on a live row.
 template <int DT, int NCMAX, int KMAX>
-__device__ void stream_block_fold(const Plan& p, HeadShared<KMAX, kRoundWaves>& sh,
-                                  SelShared& ssh, FrontShared& fs, char* ul, u32x4* wl,
-                                  int& sh_go) {
+__device__ void stream_block_fold(const Plan& p, const Plan& sp,
+                                  HeadShared<KMAX, kRoundWaves>& sh, SelShared& ssh,
+                                  FrontShared& fs, char* ul, u32x4* wl, int& sh_go) {
   constexpr int WAVES = kRoundWaves;
   constexpr int RT = resident_reg_tiles(NCMAX, true);
   constexpr int LTW = resident_lds_tiles_per_wave(NCMAX);
@@ -1001,7 +1009,7 @@ __device__ void stream_block_fold(const Plan& p, HeadShared<KMAX, kRoundWaves>& 
 #pragma unroll
     for (int q = 0; q < LP; ++q)
       load_lfrag<DT>(p, h, d, min(lds0 + wave + WAVES * (2 * q + h.half), t1 - 1), llds[q]);
-    if (!stage_inputs<DT, KMAX, false>(p, d, fs, ssh, ul, sh_go)) return;
+    if (!stage_inputs<DT, KMAX>(p, sp, d, fs, ssh, ul, sh_go)) return;
     u32x4 bfrag[NCMAX];
     load_bfrag_lds<DT, NCMAX>(p, h, ul, bfrag);
     RowAcc<KMAX> r;
@@ -1265,13 +1273,6 @@ __device__ __forceinline__ void sel_merge(const Plan& p, int d, int rows, SelSha
     sel_merge_rows<KMAX, kRoundSlicesMax / 64>(p, d, rows, sh);
 }
 
-// Out-of-line form for callers whose own registers are short (the unfolded
-// streaming loop): the merge's registers do not count against theirs, at the
-// price of reading the plan through memory.
-template <int KMAX>
-__device__ __noinline__ void sel_merge_call(const Plan& p, int d, int rows, SelShared& sh) {
-  sel_merge<KMAX>(p, d, rows, sh);
-}
 
 // The frontier of stage d + 1 from the stage-d rows in sh (a streaming
 // workgroup's share of stage_select: scores, ranks within each request's
@@ -1479,11 +1480,13 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   if (blockIdx.x < p.G) {
     __shared__ HeadShared<KMAX, kRoundWaves> hsh;
     __shared__ FrontShared fs;
+    __shared__ Plan sp;  // read by the out-of-line stage code
+    if (threadIdx.x == 0) sp = p;
     u32x4* wl = (u32x4*)(dyn + p.lds_tile_offset);
     if constexpr (FOLD)
-      stream_block_fold<DT, NCMAX, KMAX>(p, hsh, ssh, fs, dyn, wl, sh_go);
+      stream_block_fold<DT, NCMAX, KMAX>(p, sp, hsh, ssh, fs, dyn, wl, sh_go);
     else
-      stream_block<DT, NCMAX, KMAX>(p, hsh, ssh, fs, dyn, wl, sh_go);
+      stream_block<DT, NCMAX, KMAX>(p, sp, hsh, ssh, fs, dyn, wl, sh_go);
     return;
   }
 
