@@ -43,11 +43,25 @@ namespace pctree {
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+// 2^x on the transcendental unit without the library's denormal-range fixups:
+// terms that small (relative to a running maximum) do not change a sum of
+// exponentials that holds a 1.
+__device__ __forceinline__ float exp2_raw(float x) { return __builtin_amdgcn_exp2f(x); }
 constexpr float kNegBig = -3.0e38f;  // "no value yet" for running maxima
+
+// A pointer known to address global memory.  Code that is not inlined into
+// a kernel cannot tell where the plan's pointers point and would use flat
+// accesses, which also count as LDS accesses for the waits on those.
+template <typename T>
+__device__ __forceinline__ const __attribute__((address_space(1))) T* gmem(const T* ptr) {
+  return (const __attribute__((address_space(1))) T*)ptr;
+}
 
 __device__ __forceinline__ void __atomic_thread_fence_agent_acquire() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
@@ -146,7 +160,7 @@ __device__ void write_activations(const Plan& p, const State& st, int d, int req
       const int slot = rem / p.r;
       const int j = rem - slot * p.r;
       const int req = req0 + rq;
-      erow[q] = (size_t)st.front_tok[req * p.kk + slot] * p.r + j;
+      erow[q] = (size_t)min(max(st.front_tok[req * p.kk + slot], 0), p.V - 1) * p.r + j;
       urow[q] = ((size_t)req * p.kk + slot) * p.r + j;
       hrow[q] = ((size_t)req * p.B + d) * p.r + j;
     }
@@ -310,7 +324,7 @@ __device__ __forceinline__ float wave_sum_f32(float v) {
 // (m, s) pairs describe sum_i exp(z_i) = exp(m) * s; combine two of them.
 __device__ __forceinline__ void lse_combine(float& m, float& s, float om, float os) {
   const float nm = fmaxf(m, om);
-  s = s * exp2f((m - nm) * kLog2e) + os * exp2f((om - nm) * kLog2e);
+  s = s * exp2_raw((m - nm) * kLog2e) + os * exp2_raw((om - nm) * kLog2e);
   m = nm;
 }
 
@@ -531,10 +545,10 @@ __device__ __forceinline__ void tile_epilogue(const Plan& p, const HeadLane& h, 
       tmax = fmaxf(tmax, z[i]);
     }
     const float nm = fmaxf(r.m, tmax);
-    float ss = r.s * exp2f((r.m - nm) * kLog2e);
+    float ss = r.s * exp2_raw((r.m - nm) * kLog2e);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      if (tb + i < p.V) ss += exp2f((z[i] - nm) * kLog2e);
+      if (tb + i < p.V) ss += exp2_raw((z[i] - nm) * kLog2e);
     r.m = nm;
     r.s = ss;
 #pragma unroll
@@ -652,10 +666,12 @@ __device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h
       for (int i = 0; i < KMAX; ++i)
         __hip_atomic_store(dst + i, r.list[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       uint64_t* hd = (uint64_t*)(p.part_hd + o);
+#pragma unroll
+      for (int i = 0; i < kHeadKeys; ++i)
+        __hip_atomic_store(hd + i, i < KMAX ? r.list[i < KMAX ? i : 0] : 0ull, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
       const uint64_t ms = ((uint64_t)__float_as_uint(r.s) << 32) | __float_as_uint(r.m);
-      __hip_atomic_store(hd, r.list[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(hd + 1, ms, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(hd + kHeadKeys, ms, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -777,20 +793,20 @@ __device__ void compute_u(const Plan& p, const FrontShared& fs, int d, int P, ch
       const int row = e / p.r;
       const int j = e - row * p.r;
       const int req = row / P;
-      const int tok = fs.tok[req * p.kk + (row - req * P)];
+      const int tok = min(max(fs.tok[req * p.kk + (row - req * P)], 0), p.V - 1);
       const size_t eo = (size_t)tok * p.r + j;
       if (DT) {
-        const uint2 v = *(const uint2*)((const uint16_t*)p.E + eo);
+        const u32x2 v = *gmem((const u32x2*)((const uint16_t*)p.E + eo));
         ev[q][0] = v.x << 16;
         ev[q][1] = v.x & 0xffff0000u;
         ev[q][2] = v.y << 16;
         ev[q][3] = v.y & 0xffff0000u;
       } else {
-        const u32x4 v = *(const u32x4*)((const float*)p.E + eo);
+        const u32x4 v = *gmem((const u32x4*)((const float*)p.E + eo));
 #pragma unroll
         for (int i = 0; i < Q; ++i) ev[q][i] = v[i];
       }
-      hv[q] = *(const f32x4*)(p.h + ((size_t)req * p.B + d) * p.r + j);
+      hv[q] = *gmem((const f32x4*)(p.h + ((size_t)req * p.B + d) * p.r + j));
       urow[q] = row;
       j0[q] = j;
     }
@@ -836,19 +852,8 @@ template <int KMAX>
 __device__ void sel_merge(const Plan& p, int d, int rows, SelShared& sh);
 __device__ void sel_frontier(const Plan& p, FrontShared& fs, int d, int P, SelShared& sh);
 
-// The frontier of stage d from the stage-(d-1) partials and its head input in
-// LDS.  Out of line, with the plan read from an LDS copy: its registers do
-// not count against the W tiles the streaming loop keeps resident.
 template <int DT, int KMAX>
-__device__ __noinline__ void next_inputs(const Plan& p, int d, FrontShared& fs, SelShared& ssh,
-                                         char* ul) {
-  if (d > 0) {
-    const int pp = d == 1 ? 1 : p.kk;
-    sel_merge<KMAX>(p, d - 1, p.R * pp, ssh);
-    sel_frontier(p, fs, d - 1, pp, ssh);
-  }
-  compute_u<DT>(p, fs, d, d == 0 ? 1 : p.kk, ul);
-}
+__device__ void next_inputs(const Plan& lp, int d);
 
 // Everything a streaming workgroup does before its stage-d stream: wait for
 // stage d-1 to be complete, derive the stage-d frontier from its partials,
@@ -865,17 +870,17 @@ __device__ __forceinline__ bool stage_inputs(const Plan& p, const Plan& sp, int 
     __syncthreads();
     if (!sh_go) return false;
   }
-  next_inputs<DT, KMAX>(sp, d, fs, ssh, ul);
+  next_inputs<DT, KMAX>(sp, d);
   return true;
 }
 
 // The stage-0 frontier: each request's root (token 0 stands in for an invalid
 // one, whose tree is emitted empty).
 __device__ __forceinline__ void init_front(const Plan& p, FrontShared& fs) {
-  for (int req = threadIdx.x; req < p.R; req += blockDim.x) {
-    const int root = p.root[req];
-    fs.tok[req * p.kk] = root < 0 || root >= p.V ? 0 : root;
-    fs.score[req * p.kk] = 0.0f;
+  for (int i = threadIdx.x; i < p.R * p.kk; i += blockDim.x) {
+    const int root = p.root[i / p.kk];
+    fs.tok[i] = root < 0 || root >= p.V ? 0 : root;
+    fs.score[i] = 0.0f;
   }
 }
 
@@ -1175,86 +1180,127 @@ __device__ void stage_select(const Plan& p, const State& st, int d, int P, int r
 }
 
 // The top-k' children and the lse of each of the R*P (<= 16) rows of stage d
-// from the published slice partials, one wave per row.  A row's top-k' lie
-// in the k' slices with the largest best keys (any other slice is beaten k'
-// times over), so the heads of all slices are read first (with the (max,
-// sum) pairs), then the lists of those k' slices only.  Keys are unique
-// (the token is part of them), so each pop of a wave-wide maximum removes
-// exactly one entry.
+// from the published slice partials, one wave per row.  Every slice's head
+// record holds its kHeadKeys best keys and its (max, sum): k' pops of the
+// wave-wide maximum over the union of those keys give the row's top-k'
+// unless some slice gave up all of its record keys (it may hold more that
+// belong).  Then, and only then, the lists are read: a row's top-k' lie in
+// the k' slices with the largest best keys (any other slice is beaten k'
+// times over), and k' pops over those lists give the exact answer.  Keys are
+// unique (the token is part of them), so each pop removes exactly one entry.
 template <int KMAX, int HPL>
 __device__ __forceinline__ void sel_merge_rows(const Plan& p, int d, int rows, SelShared& sh) {
+  constexpr int HK = KMAX < kHeadKeys ? KMAX : kHeadKeys;  // record keys that can be real
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int nwave = blockDim.x >> 6;
   const int G = p.G;
   const int kk = p.kk;
-  const int nwin = min(kk, G);
   for (int row = wave; row < rows; row += nwave) {
     const size_t base = ((size_t)d * p.rows_max + row) * kSlicesMax;
-    uint64_t hk[HPL];
+    uint64_t hk[HPL][HK];
+    uint64_t first[HPL];
     float hm[HPL], hs[HPL];
 #pragma unroll
     for (int c = 0; c < HPL; ++c) {
-      const SliceHead v = p.part_hd[base + min(lane + 64 * c, G - 1)];
-      hk[c] = v.key;
-      hm[c] = v.m;
-      hs[c] = v.s;
+      const auto rec = gmem((const u32x4*)(p.part_hd + base + min(lane + 64 * c, G - 1)));
+      const u32x4 a = rec[0], b = rec[1];
+      const uint64_t k[3] = {((uint64_t)a.y << 32) | a.x, ((uint64_t)a.w << 32) | a.z,
+                             ((uint64_t)b.y << 32) | b.x};
+#pragma unroll
+      for (int i = 0; i < HK; ++i) hk[c][i] = k[i];
+      hm[c] = __uint_as_float(b.z);
+      hs[c] = __uint_as_float(b.w);
     }
     float m = kNegBig, s = 0.0f;
 #pragma unroll
     for (int c = 0; c < HPL; ++c) {
-      if (lane + 64 * c < G)
+      if (lane + 64 * c < G) {
         lse_combine(m, s, hm[c], hs[c]);
-      else
-        hk[c] = 0;
-    }
-    // the lane's heads sorted (descending), then k' pops of the wave maximum
+      } else {
 #pragma unroll
-    for (int c = 1; c < HPL; ++c) {
-#pragma unroll
-      for (int i = c; i > 0; --i) {
-        const uint64_t a = hk[i - 1], b = hk[i];
-        const bool sw = b > a;
-        hk[i - 1] = sw ? b : a;
-        hk[i] = sw ? a : b;
+        for (int i = 0; i < HK; ++i) hk[c][i] = 0;
       }
+      first[c] = hk[c][0];
     }
     const float M = wave_max_f32(m);
-    const float S = wave_sum_f32(s * exp2f((m - M) * kLog2e));
-    uint64_t won = 0;  // lane i keeps the i-th largest head
+    const float S = wave_sum_f32(s * exp2_raw((m - M) * kLog2e));
+    int used[HPL];
+#pragma unroll
+    for (int c = 0; c < HPL; ++c) used[c] = 0;
 #pragma unroll
     for (int it = 0; it < KMAX; ++it) {
-      if (it < nwin) {
-        const uint64_t best = wave_max_u64(hk[0]);
-        if (hk[0] == best) {
+      if (it < kk) {
+        uint64_t lm = hk[0][0];
 #pragma unroll
-          for (int c = 0; c + 1 < HPL; ++c) hk[c] = hk[c + 1];
-          hk[HPL - 1] = 0;
+        for (int c = 1; c < HPL; ++c) lm = max_u64(lm, hk[c][0]);
+        const uint64_t best = wave_max_u64(lm);
+#pragma unroll
+        for (int c = 0; c < HPL; ++c) {
+          if (hk[c][0] == best) {
+#pragma unroll
+            for (int i = 0; i + 1 < HK; ++i) hk[c][i] = hk[c][i + 1];
+            hk[c][HK - 1] = 0;
+            ++used[c];
+          }
         }
-        if (lane == it) won = best;
+        if (lane == 0) sh.rowkeys[row][it] = best;
       }
     }
-    const int myslice = lane < nwin ? min(child_key_token(won) / (p.tiles_per_slice * kTile), G - 1) : 0;
-    uint64_t lst[KMAX];
-    {
-      const uint64_t* src = p.part_key + (base + myslice) * KMAX;
+    // (pops past the union's real keys return 0 and count for every empty
+    // entry, so a slice's count can pass HK)
+    bool gave_all = false;
+    if (HK < KMAX) {
+#pragma unroll
+      for (int c = 0; c < HPL; ++c) gave_all = gave_all || used[c] >= HK;
+    }
+    if (__any(gave_all)) {
+      // the k' largest heads; lane i keeps the slice of the i-th
+      const int nwin = min(kk, G);
+#pragma unroll
+      for (int c = 1; c < HPL; ++c) {
+#pragma unroll
+        for (int i = c; i > 0; --i) {
+          const uint64_t a = first[i - 1], b = first[i];
+          const bool sw = b > a;
+          first[i - 1] = sw ? b : a;
+          first[i] = sw ? a : b;
+        }
+      }
+      uint64_t won = 0;
+#pragma unroll
+      for (int it = 0; it < KMAX; ++it) {
+        if (it < nwin) {
+          const uint64_t best = wave_max_u64(first[0]);
+          if (first[0] == best) {
+#pragma unroll
+            for (int c = 0; c + 1 < HPL; ++c) first[c] = first[c + 1];
+            first[HPL - 1] = 0;
+          }
+          if (lane == it) won = best;
+        }
+      }
+      const int myslice =
+          lane < nwin ? min(child_key_token(won) / (p.tiles_per_slice * kTile), G - 1) : 0;
+      uint64_t lst[KMAX];
+      const auto src = gmem(p.part_key) + (base + myslice) * KMAX;
 #pragma unroll
       for (int i = 0; i < KMAX; ++i) lst[i] = src[i];
       if (lane >= nwin) {
 #pragma unroll
         for (int i = 0; i < KMAX; ++i) lst[i] = 0;
       }
-    }
 #pragma unroll
-    for (int it = 0; it < KMAX; ++it) {
-      if (it < kk) {
-        const uint64_t best = wave_max_u64(lst[0]);
-        if (lst[0] == best) {
+      for (int it = 0; it < KMAX; ++it) {
+        if (it < kk) {
+          const uint64_t best = wave_max_u64(lst[0]);
+          if (lst[0] == best) {
 #pragma unroll
-          for (int i = 0; i + 1 < KMAX; ++i) lst[i] = lst[i + 1];
-          lst[KMAX - 1] = 0;
+            for (int i = 0; i + 1 < KMAX; ++i) lst[i] = lst[i + 1];
+            lst[KMAX - 1] = 0;
+          }
+          if (lane == 0) sh.rowkeys[row][it] = best;
         }
-        if (lane == 0) sh.rowkeys[row][it] = best;
       }
     }
     if (lane == 0) sh.lse[row] = M + logf(S);
@@ -1359,8 +1405,9 @@ __device__ void emit_request(const Plan& p, const State& st, int req) {
   int node = -1, dep = -1, tok = -1, pnode = -1;
   float score = 0.0f;
   if (tid < count) {
-    node = st.top_node[(size_t)req * p.N + tid];
-    dep = p.node_depth[pb + node];
+    // (clamped: an inconsistent state must not address outside the pool)
+    node = min(max(st.top_node[(size_t)req * p.N + tid], 0), p.maxpool - 1);
+    dep = min(max(p.node_depth[pb + node], 0), p.B);
     tok = p.node_tok[pb + node];
     pnode = p.node_par[pb + node];
     score = p.node_score[pb + node];
@@ -1458,6 +1505,33 @@ __device__ int wait_tags(const Plan& p, int d) {
 }
 
 
+// LDS of the persistent round kernel shared by its stage code.
+__shared__ SelShared g_sel;
+__shared__ FrontShared g_front;
+// dynamic LDS: the frontier's head input (streaming blocks), the keeper's
+// running top-N, the streaming blocks' resident W tiles
+extern __shared__ uint64_t g_dyn[];
+
+// The frontier of stage d from the stage-(d-1) partials and its head input in
+// LDS.  Out of line, with the plan read from an LDS copy: its registers do
+// not count against the W tiles the streaming loop keeps resident.  The LDS
+// objects are named directly (not passed), so that accesses stay LDS ones.
+template <int DT, int KMAX>
+__device__ __noinline__ void next_inputs(const Plan& lp, int d) {
+  // the plan into scalar registers: uniform loop bounds and addresses below
+  static_assert(sizeof(Plan) % 4 == 0, "Plan is copied word by word");
+  Plan p;
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(Plan) / 4); ++i)
+    ((int*)&p)[i] = __builtin_amdgcn_readfirstlane(((const int*)&lp)[i]);
+  if (d > 0) {
+    const int pp = d == 1 ? 1 : p.kk;
+    sel_merge<KMAX>(p, d - 1, p.R * pp, g_sel);
+    sel_frontier(p, g_front, d - 1, pp, g_sel);
+  }
+  compute_u<DT>(p, g_front, d, d == 0 ? 1 : p.kk, (char*)g_dyn);
+}
+
 // Blocks [0, G) stream one V-slice each; block G is the keeper.  Before
 // stage d every block waits for stage d-1 to be complete (its flag line,
 // raised by the workgroup that completes the arrival count) and derives the
@@ -1472,14 +1546,11 @@ __device__ int wait_tags(const Plan& p, int d) {
 template <int DT, int NCMAX, int KMAX, bool FOLD>
 __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   __shared__ int sh_go;
-  __shared__ SelShared ssh;
-  // dynamic LDS: the head input of the frontier (streaming blocks), the
-  // keeper's running top-N, the streaming blocks' resident W tiles
-  extern __shared__ uint64_t s_dyn[];
-  char* dyn = (char*)s_dyn;
+  SelShared& ssh = g_sel;
+  char* dyn = (char*)g_dyn;
   if (blockIdx.x < p.G) {
     __shared__ HeadShared<KMAX, kRoundWaves> hsh;
-    __shared__ FrontShared fs;
+    FrontShared& fs = g_front;
     __shared__ Plan sp;  // read by the out-of-line stage code
     if (threadIdx.x == 0) sp = p;
     u32x4* wl = (u32x4*)(dyn + p.lds_tile_offset);
@@ -1497,12 +1568,15 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   const State st{s_front_node, s_front_tok, s_front_score, s_top,
                  (int*)(s_top + (size_t)p.R * p.N)};
   for (int req = 0; req < p.R; ++req) init_request(p, req, threadIdx.x, blockDim.x);
+  for (int i = threadIdx.x; i < p.R * p.kk; i += blockDim.x) {
+    const int r0 = p.root[i / p.kk];
+    st.front_node[i] = 0;
+    st.front_tok[i] = r0 < 0 || r0 >= p.V ? 0 : r0;
+    st.front_score[i] = 0.0f;
+  }
   for (int req = threadIdx.x; req < p.R; req += blockDim.x) {
     const int r0 = p.root[req];
     const int root = r0 < 0 || r0 >= p.V ? 0 : r0;
-    st.front_node[req * p.kk] = 0;
-    st.front_tok[req * p.kk] = root;
-    st.front_score[req * p.kk] = 0.0f;
     st.top_key[(size_t)req * p.N] = node_key(0.0f, 0, root, 0);
     st.top_node[(size_t)req * p.N] = 0;
   }

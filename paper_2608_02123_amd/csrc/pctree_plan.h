@@ -20,11 +20,14 @@ constexpr int kNarrowRows = 16;      // frontier rows (R * k') one column block 
 constexpr int kFlagStride = 64;      // ints between two workgroups' flag words (256 B)
 
 // What a streaming workgroup publishes per (stage, row, slice) besides its
-// candidate list: the list's best key and the slice's (row max, sum of exp).
+// candidate list: the list's kHeadKeys best keys (0 past the list) and the
+// slice's (row max, sum of exp).
+constexpr int kHeadKeys = 3;
 struct SliceHead {
-  uint64_t key;
+  uint64_t key[kHeadKeys];
   float m, s;
 };
+static_assert(sizeof(SliceHead) == 32, "one SliceHead is two 16-byte loads");
 
 // Everything one round needs, passed by value to every kernel.
 struct Plan {
