@@ -285,14 +285,30 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
 
 // Keys are >= 0, so 0 (what DPP yields for lanes outside the row mask) is
 // the identity of the maximum.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, dpp<0xB1, 0xF>(v));   // quad_perm [1,0,3,2]
+  v = max(v, dpp<0x4E, 0xF>(v));   // quad_perm [2,3,0,1]
+  v = max(v, dpp<0x141, 0xF>(v));  // row_half_mirror
+  v = max(v, dpp<0x140, 0xF>(v));  // row_mirror
+  v = max(v, dpp<0x142, 0xA>(v));  // row_bcast15 into rows 1, 3
+  v = max(v, dpp<0x143, 0xC>(v));  // row_bcast31 into rows 2, 3
+  return __builtin_amdgcn_readlane(v, 63);
+}
+
+// The maximum over the wave of a u64 key: the high words decide; the low word
+// comes from the one lane holding the maximal high word, or from a second
+// reduction over the tied lanes.
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-  v = max_u64(v, dpp64<0xB1, 0xF>(v));   // quad_perm [1,0,3,2]
-  v = max_u64(v, dpp64<0x4E, 0xF>(v));   // quad_perm [2,3,0,1]
-  v = max_u64(v, dpp64<0x141, 0xF>(v));  // row_half_mirror
-  v = max_u64(v, dpp64<0x140, 0xF>(v));  // row_mirror
-  v = max_u64(v, dpp64<0x142, 0xA>(v));  // row_bcast15 into rows 1, 3
-  v = max_u64(v, dpp64<0x143, 0xC>(v));  // row_bcast31 into rows 2, 3
-  return readlane_u64(v, 63);
+  const uint32_t hi = (uint32_t)(v >> 32);
+  const uint32_t lo = (uint32_t)v;
+  const uint32_t mh = wave_max_u32(hi);
+  const uint64_t tied = __ballot(hi == mh);
+  uint32_t ml;
+  if ((tied & (tied - 1)) == 0)
+    ml = __builtin_amdgcn_readlane(lo, __builtin_ctzll(tied));
+  else
+    ml = wave_max_u32(hi == mh ? lo : 0u);
+  return ((uint64_t)mh << 32) | ml;
 }
 
 template <int CTRL, int ROWS>
