@@ -545,8 +545,18 @@ struct RowAcc {
   }
 };
 
+__device__ __forceinline__ void cas_desc(uint64_t& a, uint64_t& b) {
+  const bool sw = b > a;
+  const uint64_t hi = sw ? b : a, lo = sw ? a : b;
+  a = hi;
+  b = lo;
+}
+
 // The lane's four logits of tile t (C fragment + L_d), folded into its row's
-// online logsumexp and top-k list when `ok`.
+// online logsumexp and top-k list when `ok`.  Four new keys enter a list of
+// at least four as one sorted batch (a 4-sort, then the list merge); shorter
+// lists take them one at a time.  Only the last tile of the vocabulary can
+// hold tokens past V, and only there are they masked one by one.
 template <int DT, int KMAX>
 __device__ __forceinline__ void tile_epilogue(const Plan& p, const HeadLane& h, f32x4 acc,
                                               const uint32_t (&l)[4], int t, bool ok,
@@ -554,24 +564,53 @@ __device__ __forceinline__ void tile_epilogue(const Plan& p, const HeadLane& h, 
   if (ok) {
     const int tb = t * kTile + h.grp * 4;
     float z[4];
-    float tmax = kNegBig;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      z[i] = tb + i < p.V ? acc[i] + raw_to_f32<DT>(l[i]) : kNegBig;
-      tmax = fmaxf(tmax, z[i]);
-    }
-    const float nm = fmaxf(r.m, tmax);
-    float ss = r.s * exp2_raw((r.m - nm) * kLog2e);
+    for (int i = 0; i < 4; ++i) z[i] = acc[i] + raw_to_f32<DT>(l[i]);
+    if (tb + 3 < p.V) {
+      const float nm = fmaxf(fmaxf(r.m, fmaxf(z[0], z[1])), fmaxf(z[2], z[3]));
+      float ss = r.s * exp2_raw((r.m - nm) * kLog2e);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (tb + i < p.V) ss += exp2_raw((z[i] - nm) * kLog2e);
-    r.m = nm;
-    r.s = ss;
+      for (int i = 0; i < 4; ++i) ss += exp2_raw((z[i] - nm) * kLog2e);
+      r.m = nm;
+      r.s = ss;
+      uint64_t n[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if (tb + i < p.V) {
-        const uint64_t key = child_key(z[i], tb + i);
-        if (key > r.list[KMAX - 1]) list_insert(r.list, key);
+      for (int i = 0; i < 4; ++i) n[i] = child_key(z[i], tb + i);
+      if constexpr (KMAX >= 4) {
+        cas_desc(n[0], n[1]);
+        cas_desc(n[2], n[3]);
+        cas_desc(n[0], n[2]);
+        cas_desc(n[1], n[3]);
+        cas_desc(n[1], n[2]);
+        uint64_t b[KMAX];
+#pragma unroll
+        for (int i = 0; i < KMAX; ++i) b[i] = i < 4 ? n[i < 4 ? i : 0] : 0ull;
+        list_merge(r.list, b);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (n[i] > r.list[KMAX - 1]) list_insert(r.list, n[i]);
+      }
+    } else {
+      float tmax = kNegBig;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (tb + i >= p.V) z[i] = kNegBig;
+        tmax = fmaxf(tmax, z[i]);
+      }
+      const float nm = fmaxf(r.m, tmax);
+      float ss = r.s * exp2_raw((r.m - nm) * kLog2e);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (tb + i < p.V) ss += exp2_raw((z[i] - nm) * kLog2e);
+      r.m = nm;
+      r.s = ss;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (tb + i < p.V) {
+          const uint64_t key = child_key(z[i], tb + i);
+          if (key > r.list[KMAX - 1]) list_insert(r.list, key);
+        }
       }
     }
   }
