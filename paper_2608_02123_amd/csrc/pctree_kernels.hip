@@ -908,7 +908,7 @@ __device__ void sel_merge(const Plan& p, int d, int rows, SelShared& sh);
 __device__ void sel_frontier(const Plan& p, FrontShared& fs, int d, int P, SelShared& sh);
 
 template <int DT, int KMAX>
-__device__ void next_inputs(const Plan& lp, int d);
+__device__ __forceinline__ void next_inputs(const Plan& lp, int d);
 
 // Everything a streaming workgroup does before its stage-d stream: wait for
 // stage d-1 to be complete, derive the stage-d frontier from its partials,
@@ -1254,7 +1254,6 @@ __device__ __forceinline__ void sel_merge_rows(const Plan& p, int d, int rows, S
   for (int row = wave; row < rows; row += nwave) {
     const size_t base = ((size_t)d * p.rows_max + row) * kSlicesMax;
     uint64_t hk[HPL][HK];
-    uint64_t first[HPL];
     float hm[HPL], hs[HPL];
 #pragma unroll
     for (int c = 0; c < HPL; ++c) {
@@ -1276,7 +1275,6 @@ __device__ __forceinline__ void sel_merge_rows(const Plan& p, int d, int rows, S
 #pragma unroll
         for (int i = 0; i < HK; ++i) hk[c][i] = 0;
       }
-      first[c] = hk[c][0];
     }
     const float M = wave_max_f32(m);
     const float S = wave_sum_f32(s * exp2_raw((m - M) * kLog2e));
@@ -1310,6 +1308,13 @@ __device__ __forceinline__ void sel_merge_rows(const Plan& p, int d, int rows, S
       for (int c = 0; c < HPL; ++c) gave_all = gave_all || used[c] >= HK;
     }
     if (__any(gave_all)) {
+      // the slices' best keys again (rare: not kept in registers)
+      uint64_t first[HPL];
+#pragma unroll
+      for (int c = 0; c < HPL; ++c) {
+        const u32x4 a = *gmem((const u32x4*)(p.part_hd + base + min(lane + 64 * c, G - 1)));
+        first[c] = lane + 64 * c < G ? ((uint64_t)a.y << 32) | a.x : 0ull;
+      }
       // the k' largest heads; lane i keeps the slice of the i-th
       const int nwin = min(kk, G);
 #pragma unroll
@@ -1567,24 +1572,42 @@ __shared__ FrontShared g_front;
 // running top-N, the streaming blocks' resident W tiles
 extern __shared__ uint64_t g_dyn[];
 
-// The frontier of stage d from the stage-(d-1) partials and its head input in
-// LDS.  Out of line, with the plan read from an LDS copy: its registers do
-// not count against the W tiles the streaming loop keeps resident.  The LDS
-// objects are named directly (not passed), so that accesses stay LDS ones.
-template <int DT, int KMAX>
-__device__ __noinline__ void next_inputs(const Plan& lp, int d) {
-  // the plan into scalar registers: uniform loop bounds and addresses below
+// The plan in scalar registers (read from its LDS copy): uniform loop bounds
+// and addresses in the out-of-line stage code below.
+__device__ __forceinline__ Plan scalar_plan(const Plan& lp) {
   static_assert(sizeof(Plan) % 4 == 0, "Plan is copied word by word");
   Plan p;
 #pragma unroll
   for (int i = 0; i < (int)(sizeof(Plan) / 4); ++i)
     ((int*)&p)[i] = __builtin_amdgcn_readfirstlane(((const int*)&lp)[i]);
-  if (d > 0) {
-    const int pp = d == 1 ? 1 : p.kk;
-    sel_merge<KMAX>(p, d - 1, p.R * pp, g_sel);
-    sel_frontier(p, g_front, d - 1, pp, g_sel);
-  }
+  return p;
+}
+
+// The stage code runs out of line, as two calls with the plan read from an
+// LDS copy: their registers do not count against the W tiles the streaming
+// loop keeps resident (the smaller each call, the fewer of the caller's
+// values it clobbers).  The LDS objects are named directly (not passed), so
+// that accesses stay LDS ones.
+template <int KMAX>
+__device__ __noinline__ void merge_call(const Plan& lp, int d) {
+  const Plan p = scalar_plan(lp);
+  const int pp = d == 1 ? 1 : p.kk;
+  sel_merge<KMAX>(p, d - 1, p.R * pp, g_sel);
+}
+
+template <int DT>
+__device__ __noinline__ void frontier_call(const Plan& lp, int d) {
+  const Plan p = scalar_plan(lp);
+  if (d > 0) sel_frontier(p, g_front, d - 1, d == 1 ? 1 : p.kk, g_sel);
   compute_u<DT>(p, g_front, d, d == 0 ? 1 : p.kk, (char*)g_dyn);
+}
+
+// The frontier of stage d from the stage-(d-1) partials and its head input in
+// LDS.
+template <int DT, int KMAX>
+__device__ __forceinline__ void next_inputs(const Plan& lp, int d) {
+  if (d > 0) merge_call<KMAX>(lp, d);
+  frontier_call<DT>(lp, d);
 }
 
 // Blocks [0, G) stream one V-slice each; block G is the keeper.  Before
