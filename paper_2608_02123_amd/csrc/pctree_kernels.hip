@@ -23,7 +23,7 @@
 //
 // Ordering keys are unique 64-bit integers, so every selection is exact and
 // deterministic:
-//   child key = ord(z)     << 32 | ~token                          (z desc, token asc)
+//   child key = ord(z)     << 30 | (2^20-1-token) << 10            (z desc, token asc)
 //   node key  = ord(score) << 32 | (63-depth) << 26 | (2^20-1-token) << 6 | (63-slot)
 //                                         (score desc, depth asc, token asc, slot asc)
 // where ord() maps a float onto an unsigned integer of the same order (-0 -> +0).
@@ -77,14 +77,19 @@ __device__ __forceinline__ float f32_unord(uint32_t o) {
   return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
 }
 
+// Child keys leave their two top bits clear: read as an IEEE double, every
+// key is non-negative, finite and (but 0) normal, and double order is key
+// order, so the lists compare and swap them with v_max_f64 / v_min_f64.
 __device__ __forceinline__ uint64_t child_key(float z, int tok) {
-  return ((uint64_t)f32_ord(z) << 32) | (uint64_t)(~(uint32_t)tok);
+  return ((uint64_t)f32_ord(z) << 30) | ((uint64_t)(0xFFFFF - tok) << 10);
 }
 
-__device__ __forceinline__ int child_key_token(uint64_t key) { return (int)(~(uint32_t)key); }
+__device__ __forceinline__ int child_key_token(uint64_t key) {
+  return 0xFFFFF - (int)((key >> 10) & 0xFFFFF);
+}
 
 __device__ __forceinline__ float child_key_value(uint64_t key) {
-  return f32_unord((uint32_t)(key >> 32));
+  return f32_unord((uint32_t)(key >> 30));
 }
 
 __device__ __forceinline__ uint64_t node_key(float score, int depth, int tok, int slot) {
@@ -186,15 +191,24 @@ __device__ void write_activations(const Plan& p, const State& st, int d, int req
 // ---------------------------------------------------------------------------
 // sorted (descending) fixed-length candidate lists held in registers
 // ---------------------------------------------------------------------------
+// Larger / smaller of two child keys (see child_key) on the double ALU.
+__device__ __forceinline__ uint64_t key_max(uint64_t a, uint64_t b) {
+  return (uint64_t)__double_as_longlong(
+      __builtin_fmax(__longlong_as_double((long long)a), __longlong_as_double((long long)b)));
+}
+__device__ __forceinline__ uint64_t key_min(uint64_t a, uint64_t b) {
+  return (uint64_t)__double_as_longlong(
+      __builtin_fmin(__longlong_as_double((long long)a), __longlong_as_double((long long)b)));
+}
+
 template <int K>
 __device__ __forceinline__ void list_insert(uint64_t (&l)[K], uint64_t key) {
   l[K - 1] = key;
 #pragma unroll
   for (int i = K - 1; i > 0; --i) {
     const uint64_t a = l[i - 1], b = l[i];
-    const bool s = b > a;
-    l[i - 1] = s ? b : a;
-    l[i] = s ? a : b;
+    l[i - 1] = key_max(a, b);
+    l[i] = key_min(a, b);
   }
 }
 
@@ -203,19 +217,34 @@ __device__ __forceinline__ void list_insert(uint64_t (&l)[K], uint64_t key) {
 template <int K>
 __device__ __forceinline__ void list_merge(uint64_t (&a)[K], const uint64_t (&b)[K]) {
 #pragma unroll
-  for (int i = 0; i < K; ++i) {
-    const uint64_t x = a[i], y = b[K - 1 - i];
-    a[i] = x > y ? x : y;
-  }
+  for (int i = 0; i < K; ++i) a[i] = key_max(a[i], b[K - 1 - i]);
 #pragma unroll
   for (int j = K / 2; j > 0; j >>= 1) {
 #pragma unroll
     for (int i = 0; i < K; ++i) {
       if ((i & j) == 0) {
         const uint64_t x = a[i], y = a[i + j];
-        const bool s = y > x;
-        a[i] = s ? y : x;
-        a[i + j] = s ? x : y;
+        a[i] = key_max(x, y);
+        a[i + j] = key_min(x, y);
+      }
+    }
+  }
+}
+
+// a <- top-K of (a u n), n four keys sorted descending (K >= 4): only the
+// last four entries of a can give way, then half-cleaners sort the result.
+template <int K>
+__device__ __forceinline__ void list_merge4(uint64_t (&a)[K], const uint64_t (&n)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) a[K - 4 + i] = key_max(a[K - 4 + i], n[3 - i]);
+#pragma unroll
+  for (int j = K / 2; j > 0; j >>= 1) {
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+      if ((i & j) == 0) {
+        const uint64_t x = a[i], y = a[i + j];
+        a[i] = key_max(x, y);
+        a[i + j] = key_min(x, y);
       }
     }
   }
@@ -546,8 +575,7 @@ struct RowAcc {
 };
 
 __device__ __forceinline__ void cas_desc(uint64_t& a, uint64_t& b) {
-  const bool sw = b > a;
-  const uint64_t hi = sw ? b : a, lo = sw ? a : b;
+  const uint64_t hi = key_max(a, b), lo = key_min(a, b);
   a = hi;
   b = lo;
 }
@@ -582,10 +610,7 @@ __device__ __forceinline__ void tile_epilogue(const Plan& p, const HeadLane& h, 
         cas_desc(n[0], n[2]);
         cas_desc(n[1], n[3]);
         cas_desc(n[1], n[2]);
-        uint64_t b[KMAX];
-#pragma unroll
-        for (int i = 0; i < KMAX; ++i) b[i] = i < 4 ? n[i < 4 ? i : 0] : 0ull;
-        list_merge(r.list, b);
+        list_merge4(r.list, n);
       } else {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -1286,7 +1311,7 @@ __device__ __forceinline__ void sel_merge_rows(const Plan& p, int d, int rows, S
       if (it < kk) {
         uint64_t lm = hk[0][0];
 #pragma unroll
-        for (int c = 1; c < HPL; ++c) lm = max_u64(lm, hk[c][0]);
+        for (int c = 1; c < HPL; ++c) lm = key_max(lm, hk[c][0]);
         const uint64_t best = wave_max_u64(lm);
 #pragma unroll
         for (int c = 0; c < HPL; ++c) {
