@@ -137,7 +137,7 @@ size_t carve_workspace(Plan& p, char* base) {
   p.part_key = (uint64_t*)take(parts * p.kmax * sizeof(uint64_t));
   p.part_hd = (SliceHead*)take(parts * sizeof(SliceHead));
   p.req_bad = (int*)take(R * sizeof(int));
-  p.tags = (uint64_t*)take((size_t)p.stages * kSlicesMax * sizeof(uint64_t));
+  p.front_w = (uint64_t*)take((size_t)p.stages * p.rows_max * sizeof(uint64_t));
   return off;
 }
 

@@ -33,8 +33,6 @@
 
 #include <algorithm>
 #include <atomic>
-#include <chrono>
-#include <random>
 
 #define PCTREE_EMIT_MAX_N 256
 #define PCTREE_MASK_MAX_N 1024
@@ -767,36 +765,34 @@ __device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h
     list_merge_pair<32>(r.list);
     lse_combine_pair<32>(r.m, r.s);
     if (h.grp == 0 && h.row_ok && h.lead) {
-      // write-through (agent-coherent) stores: the arrival count that
-      // follows needs no L2 write-back
+      // tagged words, stored write-through at agent scope: each one is
+      // valid on its own once it lands (keys have their low kTagBits clear)
       const size_t o = ((size_t)stage * p.rows_max + h.row) * kSlicesMax + slice;
       uint64_t* dst = p.part_key + o * KMAX;
 #pragma unroll
       for (int i = 0; i < KMAX; ++i)
-        __hip_atomic_store(dst + i, r.list[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(dst + i, r.list[i] | p.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       uint64_t* hd = (uint64_t*)(p.part_hd + o);
 #pragma unroll
       for (int i = 0; i < kHeadKeys; ++i)
-        __hip_atomic_store(hd + i, i < KMAX ? r.list[i < KMAX ? i : 0] : 0ull, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-      const uint64_t ms = ((uint64_t)__float_as_uint(r.s) << 32) | __float_as_uint(r.m);
-      __hip_atomic_store(hd + kHeadKeys, ms, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(hd + i, (i < KMAX ? r.list[i < KMAX ? i : 0] : 0ull) | p.tag,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // the sum relative to the best logit (r.m is the logit of list[0])
+      const uint64_t sw = ((uint64_t)p.tag << 32) | __float_as_uint(r.s);
+      __hip_atomic_store(hd + kHeadKeys, sw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
 
-// Announce this slice's stage-d partial (wave 0 stored it write-through):
-// once those stores have completed they are visible at agent scope, and the
-// slice's tag for the stage is set to the call's epoch.  Readers poll the tags.
-__device__ __forceinline__ void publish_tag(const Plan& p, int d, int slice) {
-  if (threadIdx.x < 64) {
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_waitcnt(0);
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    if (threadIdx.x == 0)
-      __hip_atomic_store(p.tags + (size_t)d * kSlicesMax + slice, p.epoch, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-  }
+// Published words of this call (see SliceHead).
+__device__ __forceinline__ bool key_tagged(const Plan& p, uint64_t w) {
+  return ((uint32_t)w & kTagMask) == p.tag;
+}
+__device__ __forceinline__ bool sum_tagged(const Plan& p, uint64_t w) {
+  return (uint32_t)(w >> 32) == p.tag;
+}
+__device__ __forceinline__ uint64_t load_agent(const uint64_t* ptr) {
+  return __hip_atomic_load(ptr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Stream one slice of W for one block of 16 frontier rows (multi-launch form):
@@ -852,8 +848,6 @@ __device__ __forceinline__ void head_slice(const Plan& p, int d, int P, int cb, 
   }
   publish_partial<KMAX, WAVES>(p, h, 0, slice, r, sh);
 }
-
-__device__ int wait_tags(const Plan& p, int d);
 
 // Tiles a streaming block of the persistent kernel keeps on chip for the
 // whole round: RT per wave in registers and up to LTW per wave in LDS.
@@ -959,30 +953,44 @@ __device__ __forceinline__ void load_bfrag_lds(const Plan& p, const HeadLane& h,
 }
 
 
-struct SelShared;
-template <int KMAX>
-__device__ void sel_merge(const Plan& p, int d, int rows, SelShared& sh);
-__device__ void sel_frontier(const Plan& p, FrontShared& fs, int d, int P, SelShared& sh);
+template <int DT>
+__device__ __noinline__ void frontier_call(const Plan& lp, int d);
 
-template <int DT, int KMAX>
-__device__ __forceinline__ void next_inputs(const Plan& lp, int d);
+// Wave 0 waits for the stage-d frontier that the keeper publishes (R*k'
+// words, each carrying the call's tag: score bits << 32 | token << kTagBits
+// | tag) and puts its tokens into fs.  Polls with agent-coherent loads,
+// bounded by p.spin_ticks of the device wall clock: returns 0 on a timeout.
+__device__ __forceinline__ int wait_frontier(const Plan& p, int d, FrontShared& fs) {
+  const int lane = threadIdx.x & 63;
+  const int n = p.R * p.kk;  // <= kNarrowRows
+  const uint64_t* src = p.front_w + (size_t)d * p.rows_max + min(lane, n - 1);
+  const long long t0 = wall_clock64();
+  uint64_t w;
+  for (;;) {
+    w = load_agent(src);
+    if (__all(key_tagged(p, w))) break;
+    if (wall_clock64() - t0 > p.spin_ticks) return 0;
+    __builtin_amdgcn_s_sleep(1);
+  }
+  if (lane < n) fs.tok[lane] = min((int)((uint32_t)w >> kTagBits), p.V - 1);
+  return 1;
+}
 
 // Everything a streaming workgroup does before its stage-d stream: wait for
-// stage d-1 to be complete, derive the stage-d frontier from its partials,
-// and build the head input in LDS.  Returns false if the round was aborted.
+// the stage-d frontier and build its head input in LDS.  Returns false if
+// the round was abandoned.
 template <int DT, int KMAX>
 __device__ __forceinline__ bool stage_inputs(const Plan& p, const Plan& sp, int d,
-                                             FrontShared& fs, SelShared& ssh, char* ul,
-                                             int& sh_go) {
+                                             FrontShared& fs, int& sh_go) {
   if (d > 0) {
     if (threadIdx.x < 64) {
-      const int ok = wait_tags(p, d - 1);
+      const int ok = wait_frontier(p, d, fs);
       if (threadIdx.x == 0) sh_go = ok;
     }
     __syncthreads();
     if (!sh_go) return false;
   }
-  next_inputs<DT, KMAX>(sp, d);
+  frontier_call<DT>(sp, d);
   return true;
 }
 
@@ -1002,7 +1010,7 @@ __device__ __forceinline__ void init_front(const Plan& p, FrontShared& fs) {
 // selection + head stream + partial publication.
 template <int DT, int NCMAX, int KMAX>
 __device__ void stream_block(const Plan& p, const Plan& sp, HeadShared<KMAX, kRoundWaves>& sh,
-                             SelShared& ssh, FrontShared& fs, char* ul, u32x4* wl, int& sh_go) {
+                             FrontShared& fs, char* ul, u32x4* wl, int& sh_go) {
   constexpr int WAVES = kRoundWaves;
   constexpr int RT = resident_reg_tiles(NCMAX);
   constexpr int LTW = resident_lds_tiles_per_wave(NCMAX);
@@ -1044,7 +1052,7 @@ __device__ void stream_block(const Plan& p, const Plan& sp, HeadShared<KMAX, kRo
 #pragma unroll
     for (int q = 0; q < LTW; ++q)
       load_lfrag<DT>(p, h, d, min(lds0 + wave + WAVES * q, t1 - 1), llds[q]);
-    if (!stage_inputs<DT, KMAX>(p, sp, d, fs, ssh, ul, sh_go)) return;
+    if (!stage_inputs<DT, KMAX>(p, sp, d, fs, sh_go)) return;
     u32x4 bfrag[NCMAX];
     load_bfrag_lds<DT, NCMAX>(p, h, ul, bfrag);
     RowAcc<KMAX> r;
@@ -1071,7 +1079,6 @@ __device__ void stream_block(const Plan& p, const Plan& sp, HeadShared<KMAX, kRo
       tile_step<DT, NCMAX, KMAX>(p, h, T.a, bfrag, T.l, t, r);
     }
     publish_partial<KMAX, WAVES>(p, h, d, slice, r, sh);
-    publish_tag(p, d, slice);
   }
 }
 
@@ -1080,8 +1087,8 @@ __device__ void stream_block(const Plan& p, const Plan& sp, HeadShared<KMAX, kRo
 // HeadLane), so every lane's epilogue works on a live row.
 template <int DT, int NCMAX, int KMAX>
 __device__ void stream_block_fold(const Plan& p, const Plan& sp,
-                                  HeadShared<KMAX, kRoundWaves>& sh, SelShared& ssh,
-                                  FrontShared& fs, char* ul, u32x4* wl, int& sh_go) {
+                                  HeadShared<KMAX, kRoundWaves>& sh, FrontShared& fs, char* ul,
+                                  u32x4* wl, int& sh_go) {
   constexpr int WAVES = kRoundWaves;
   constexpr int RT = resident_reg_tiles(NCMAX, true);
   constexpr int LTW = resident_lds_tiles_per_wave(NCMAX);
@@ -1126,7 +1133,7 @@ __device__ void stream_block_fold(const Plan& p, const Plan& sp,
 #pragma unroll
     for (int q = 0; q < LP; ++q)
       load_lfrag<DT>(p, h, d, min(lds0 + wave + WAVES * (2 * q + h.half), t1 - 1), llds[q]);
-    if (!stage_inputs<DT, KMAX>(p, sp, d, fs, ssh, ul, sh_go)) return;
+    if (!stage_inputs<DT, KMAX>(p, sp, d, fs, sh_go)) return;
     u32x4 bfrag[NCMAX];
     load_bfrag_lds<DT, NCMAX>(p, h, ul, bfrag);
     RowAcc<KMAX> r;
@@ -1165,7 +1172,6 @@ __device__ void stream_block_fold(const Plan& p, const Plan& sp,
       tile_pair_step<DT, NCMAX, KMAX>(p, h, a0, a1, bfrag, l, tl, h.half ? okb : true, r);
     }
     publish_partial<KMAX, WAVES, true>(p, h, d, slice, r, sh);
-    publish_tag(p, d, slice);
   }
 }
 
@@ -1195,6 +1201,7 @@ struct SelShared {
   __attribute__((aligned(16))) uint64_t ckey[256];  // node keys of the stage's candidates
   int rank[256];
   __attribute__((aligned(16))) uint64_t tkey[PCTREE_EMIT_MAX_N];  // a request's top-N keys
+  int abort;  // a wait of the selection timed out
 };
 
 // Candidates of the P rows of each request in [req0, req0 + nreq), whose
@@ -1204,7 +1211,7 @@ struct SelShared {
 // into the running global top-N (Sec. 4.2) and write the next head input.
 // Needs blockDim >= 512 and nreq * P * k' <= 256.
 __device__ void stage_select(const Plan& p, const State& st, int d, int P, int req0, int nreq,
-                             SelShared& sh, bool act) {
+                             SelShared& sh, bool act, bool bcast) {
   const int tid = threadIdx.x;
   const int kk = p.kk;
   const int per_req = P * kk;
@@ -1247,6 +1254,11 @@ __device__ void stage_select(const Plan& p, const State& st, int d, int P, int r
     const int ci = tid - rq * per_req;
     const int req = req0 + rq;
     const int slot = sh.rank[tid];
+    if (bcast)  // the streaming workgroups wait for these words
+      __hip_atomic_store(p.front_w + (size_t)(d + 1) * p.rows_max + req * kk + slot,
+                         ((uint64_t)__float_as_uint(score) << 32) |
+                             ((uint64_t)tok << kTagBits) | p.tag,
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     st.front_node[req * kk + slot] = nbase + ci;
     st.front_tok[req * kk + slot] = tok;
     st.front_score[req * kk + slot] = score;
@@ -1292,46 +1304,73 @@ __device__ void stage_select(const Plan& p, const State& st, int d, int P, int r
 }
 
 // The top-k' children and the lse of each of the R*P (<= 16) rows of stage d
-// from the published slice partials, one wave per row.  Every slice's head
-// record holds its kHeadKeys best keys and its (max, sum): k' pops of the
-// wave-wide maximum over the union of those keys give the row's top-k'
-// unless some slice gave up all of its record keys (it may hold more that
-// belong).  Then, and only then, the lists are read: a row's top-k' lie in
-// the k' slices with the largest best keys (any other slice is beaten k'
-// times over), and k' pops over those lists give the exact answer.  Keys are
-// unique (the token is part of them), so each pop removes exactly one entry.
+// from the published slice partials, one wave per row, as the words land:
+// every word carries the call's tag, so the wave re-reads (agent-coherent
+// loads) the records that are not complete yet until all are.  Every slice's
+// record holds its kHeadKeys best keys and its sum of exp: k' pops of the
+// wave-wide maximum over the union of those keys give the row's top-k' unless
+// some slice gave up all of its record keys (it may hold more that belong).
+// Then, and only then, the lists are read: a row's top-k' lie in the k'
+// slices with the largest best keys (any other slice is beaten k' times
+// over), and k' pops over those lists give the exact answer.  Keys are unique
+// (the token is part of them), so each pop removes exactly one entry.
+// Returns false if a wait ran past p.spin_ticks (the round is abandoned).
 template <int KMAX, int HPL>
-__device__ __forceinline__ void sel_merge_rows(const Plan& p, int d, int rows, SelShared& sh) {
+__device__ __forceinline__ bool sel_merge_rows(const Plan& p, int d, int rows, SelShared& sh) {
   constexpr int HK = KMAX < kHeadKeys ? KMAX : kHeadKeys;  // record keys that can be real
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int nwave = blockDim.x >> 6;
   const int G = p.G;
   const int kk = p.kk;
-  for (int row = wave; row < rows; row += nwave) {
+  bool alive = true;
+  for (int row = wave; row < rows && alive; row += nwave) {
     const size_t base = ((size_t)d * p.rows_max + row) * kSlicesMax;
-    uint64_t hk[HPL][HK];
-    float hm[HPL], hs[HPL];
+    uint64_t hk[HPL][HK], first[HPL];
+    float hs[HPL];
+    bool have[HPL];
 #pragma unroll
     for (int c = 0; c < HPL; ++c) {
-      const auto rec = gmem((const u32x4*)(p.part_hd + base + min(lane + 64 * c, G - 1)));
-      const u32x4 a = rec[0], b = rec[1];
-      const uint64_t k[3] = {((uint64_t)a.y << 32) | a.x, ((uint64_t)a.w << 32) | a.z,
-                             ((uint64_t)b.y << 32) | b.x};
+      have[c] = lane + 64 * c >= G;  // no slice: nothing to wait for
 #pragma unroll
-      for (int i = 0; i < HK; ++i) hk[c][i] = k[i];
-      hm[c] = __uint_as_float(b.z);
-      hs[c] = __uint_as_float(b.w);
+      for (int i = 0; i < HK; ++i) hk[c][i] = 0;
+      hs[c] = 0.0f;
     }
+    const long long t0 = wall_clock64();
+    for (;;) {
+#pragma unroll
+      for (int c = 0; c < HPL; ++c) {
+        if (!have[c]) {
+          const uint64_t* rec = (const uint64_t*)(p.part_hd + base + lane + 64 * c);
+          uint64_t w[kHeadKeys + 1];
+#pragma unroll
+          for (int i = 0; i <= kHeadKeys; ++i) w[i] = load_agent(rec + i);
+          bool ok = sum_tagged(p, w[kHeadKeys]);
+#pragma unroll
+          for (int i = 0; i < kHeadKeys; ++i) ok = ok && key_tagged(p, w[i]);
+          have[c] = ok;
+#pragma unroll
+          for (int i = 0; i < HK; ++i) hk[c][i] = w[i];
+          hs[c] = __uint_as_float((uint32_t)w[kHeadKeys]);
+        }
+      }
+      bool all = true;
+#pragma unroll
+      for (int c = 0; c < HPL; ++c) all = all && have[c];
+      if (__all(all)) break;
+      if (wall_clock64() - t0 > p.spin_ticks) {
+        alive = false;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    if (!alive) break;
+    // lse over the slices: each sum is relative to the slice's best logit
     float m = kNegBig, s = 0.0f;
 #pragma unroll
     for (int c = 0; c < HPL; ++c) {
-      if (lane + 64 * c < G) {
-        lse_combine(m, s, hm[c], hs[c]);
-      } else {
-#pragma unroll
-        for (int i = 0; i < HK; ++i) hk[c][i] = 0;
-      }
+      first[c] = hk[c][0];
+      if (lane + 64 * c < G) lse_combine(m, s, child_key_value(hk[c][0]), hs[c]);
     }
     const float M = wave_max_f32(m);
     const float S = wave_sum_f32(s * exp2_raw((m - M) * kLog2e));
@@ -1365,14 +1404,7 @@ __device__ __forceinline__ void sel_merge_rows(const Plan& p, int d, int rows, S
       for (int c = 0; c < HPL; ++c) gave_all = gave_all || used[c] >= HK;
     }
     if (__any(gave_all)) {
-      // the slices' best keys again (rare: not kept in registers)
-      uint64_t first[HPL];
-#pragma unroll
-      for (int c = 0; c < HPL; ++c) {
-        const u32x4 a = *gmem((const u32x4*)(p.part_hd + base + min(lane + 64 * c, G - 1)));
-        first[c] = lane + 64 * c < G ? ((uint64_t)a.y << 32) | a.x : 0ull;
-      }
-      // the k' largest heads; lane i keeps the slice of the i-th
+      // the k' largest best keys; lane i keeps the slice of the i-th
       const int nwin = min(kk, G);
 #pragma unroll
       for (int c = 1; c < HPL; ++c) {
@@ -1399,10 +1431,30 @@ __device__ __forceinline__ void sel_merge_rows(const Plan& p, int d, int rows, S
       }
       const int myslice =
           lane < nwin ? min(child_key_token(won) / (p.tiles_per_slice * kTile), G - 1) : 0;
+      const uint64_t* src = p.part_key + (base + myslice) * KMAX;
       uint64_t lst[KMAX];
-      const auto src = gmem(p.part_key) + (base + myslice) * KMAX;
 #pragma unroll
-      for (int i = 0; i < KMAX; ++i) lst[i] = src[i];
+      for (int i = 0; i < KMAX; ++i) lst[i] = 0;
+      bool got = lane >= nwin;
+      const long long t1 = wall_clock64();
+      for (;;) {
+        if (!got) {
+          bool ok = true;
+#pragma unroll
+          for (int i = 0; i < KMAX; ++i) {
+            lst[i] = load_agent(src + i);
+            ok = ok && key_tagged(p, lst[i]);
+          }
+          got = ok;
+        }
+        if (__all(got)) break;
+        if (wall_clock64() - t1 > p.spin_ticks) {
+          alive = false;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      if (!alive) break;
       if (lane >= nwin) {
 #pragma unroll
         for (int i = 0; i < KMAX; ++i) lst[i] = 0;
@@ -1422,56 +1474,19 @@ __device__ __forceinline__ void sel_merge_rows(const Plan& p, int d, int rows, S
     }
     if (lane == 0) sh.lse[row] = M + logf(S);
   }
+  if (!alive && lane == 0) sh.abort = 1;
   __syncthreads();
+  return sh.abort == 0;
 }
 
 // The persistent form uses at most kRoundSlicesMax slices (one per CU).
 template <int KMAX>
-__device__ __forceinline__ void sel_merge(const Plan& p, int d, int rows, SelShared& sh) {
-  if (p.G <= 64)
-    sel_merge_rows<KMAX, 1>(p, d, rows, sh);
-  else if (p.G <= 128)
-    sel_merge_rows<KMAX, 2>(p, d, rows, sh);
-  else
-    sel_merge_rows<KMAX, kRoundSlicesMax / 64>(p, d, rows, sh);
+__device__ __forceinline__ bool sel_merge(const Plan& p, int d, int rows, SelShared& sh) {
+  if (p.G <= 64) return sel_merge_rows<KMAX, 1>(p, d, rows, sh);
+  if (p.G <= 128) return sel_merge_rows<KMAX, 2>(p, d, rows, sh);
+  return sel_merge_rows<KMAX, kRoundSlicesMax / 64>(p, d, rows, sh);
 }
 
-
-// The frontier of stage d + 1 from the stage-d rows in sh (a streaming
-// workgroup's share of stage_select: scores, ranks within each request's
-// layer, the k' best become the new slots).
-__device__ void sel_frontier(const Plan& p, FrontShared& fs, int d, int P, SelShared& sh) {
-  const int tid = threadIdx.x;
-  const int kk = p.kk;
-  const int per_req = P * kk;
-  const int ncand = p.R * per_req;
-  int tok = 0;
-  float score = 0.0f;
-  if (tid < ncand) {
-    const int rq = tid / per_req;
-    const int ci = tid - rq * per_req;
-    const int pr = ci / kk;
-    const int j = ci - pr * kk;
-    const int lrow = rq * P + pr;
-    const uint64_t ck = sh.rowkeys[lrow][j];
-    tok = min(max(child_key_token(ck), 0), p.V - 1);
-    score = fs.score[rq * kk + pr] + (child_key_value(ck) - sh.lse[lrow]);
-    sh.ckey[tid] = node_key(score, d + 1, tok, pr);
-  }
-  __syncthreads();
-  int rank = kk;
-  if (tid < ncand) {
-    const int rq = tid / per_req;
-    rank = count_greater(sh.ckey + rq * per_req, per_req, sh.ckey[tid]);
-  }
-  __syncthreads();  // every frontier slot was read above
-  if (tid < ncand && rank < kk) {
-    const int rq = tid / per_req;
-    fs.tok[rq * kk + rank] = tok;
-    fs.score[rq * kk + rank] = score;
-  }
-  __syncthreads();
-}
 
 // ---------------------------------------------------------------------------
 // emission in canonical order (+ optional ancestor mask)
@@ -1592,36 +1607,6 @@ __device__ void emit_request(const Plan& p, const State& st, int req) {
   __syncthreads();
 }
 
-// Wave 0 waits until every slice's stage-d tag holds this call's epoch, then
-// acquires (the partials were stored write-through before the tags).  Polls
-// use relaxed agent-scope loads (an acquire per poll would invalidate the L2
-// each time).  Bounded by p.spin_ticks of the device wall clock: returns 0 on
-// a timeout and the workgroup leaves the round, which then ends without
-// emission (count stays -1).
-__device__ int wait_tags(const Plan& p, int d) {
-  constexpr int TPL = kRoundSlicesMax / 64;
-  const int lane = threadIdx.x & 63;
-  const uint64_t* tg = p.tags + (size_t)d * kSlicesMax;
-  const long long t0 = wall_clock64();
-  for (;;) {
-    uint64_t v[TPL];
-#pragma unroll
-    for (int c = 0; c < TPL; ++c)
-      v[c] = __hip_atomic_load(tg + min(lane + 64 * c, p.G - 1), __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-    bool ok = true;
-#pragma unroll
-    for (int c = 0; c < TPL; ++c) ok = ok && v[c] == p.epoch;
-    if (__all(ok)) {
-      __atomic_thread_fence_agent_acquire();
-      return 1;
-    }
-    if (wall_clock64() - t0 > p.spin_ticks) return 0;
-    __builtin_amdgcn_s_sleep(1);
-  }
-}
-
-
 // LDS of the persistent round kernel shared by its stage code.
 __shared__ SelShared g_sel;
 __shared__ FrontShared g_front;
@@ -1640,44 +1625,26 @@ __device__ __forceinline__ Plan scalar_plan(const Plan& lp) {
   return p;
 }
 
-// The stage code runs out of line, as two calls with the plan read from an
-// LDS copy: their registers do not count against the W tiles the streaming
-// loop keeps resident (the smaller each call, the fewer of the caller's
-// values it clobbers).  The LDS objects are named directly (not passed), so
-// that accesses stay LDS ones.
-template <int KMAX>
-__device__ __noinline__ void merge_call(const Plan& lp, int d) {
-  const Plan p = scalar_plan(lp);
-  const int pp = d == 1 ? 1 : p.kk;
-  sel_merge<KMAX>(p, d - 1, p.R * pp, g_sel);
-}
-
+// The head-input code runs out of line with the plan read from an LDS copy:
+// its registers do not count against the W tiles the streaming loop keeps
+// resident.  The LDS objects are named directly (not passed), so that
+// accesses stay LDS ones.
 template <int DT>
 __device__ __noinline__ void frontier_call(const Plan& lp, int d) {
   const Plan p = scalar_plan(lp);
-  if (d > 0) sel_frontier(p, g_front, d - 1, d == 1 ? 1 : p.kk, g_sel);
   compute_u<DT>(p, g_front, d, d == 0 ? 1 : p.kk, (char*)g_dyn);
 }
 
-// The frontier of stage d from the stage-(d-1) partials and its head input in
-// LDS.
-template <int DT, int KMAX>
-__device__ __forceinline__ void next_inputs(const Plan& lp, int d) {
-  if (d > 0) merge_call<KMAX>(lp, d);
-  frontier_call<DT>(lp, d);
-}
-
-// Blocks [0, G) stream one V-slice each; block G is the keeper.  Before
-// stage d every block waits for stage d-1 to be complete (its flag line,
-// raised by the workgroup that completes the arrival count) and derives the
-// stage-d frontier from the published partials itself, so no head input
-// travels between workgroups.  The keeper makes the same selection and in
-// addition keeps the pool, the trace and the running top-N (in LDS), and
-// emits the tree after the last stage.  Slice partials are stored
-// write-through at agent scope and a block waits for those stores to complete
-// before it counts its arrival; a waiting block's thread 0 polls with relaxed
-// loads and acquires once, ordered before every wave's later loads by the
-// next workgroup barrier.
+// Blocks [0, G) stream one V-slice each; block G is the keeper.  A streaming
+// block publishes the stage-d partial of its slice as tagged words (no
+// ordering, no flag) and, for stage d+1, waits for the frontier words that
+// the keeper publishes.  The keeper waits for all slice partials of stage d
+// (re-reading the records that are not complete yet), merges them, selects
+// the stage-(d+1) frontier and publishes it first; then it keeps the pool,
+// the trace and the running top-N (in LDS), and emits the tree after the last
+// stage.  All cross-workgroup words are written and read with agent-coherent
+// (L2-bypassing) accesses; each word is valid on its own, so no fence is
+// needed anywhere.  The tagged buffers are cleared before every call.
 template <int DT, int NCMAX, int KMAX, bool FOLD>
 __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   __shared__ int sh_go;
@@ -1690,9 +1657,9 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
     if (threadIdx.x == 0) sp = p;
     u32x4* wl = (u32x4*)(dyn + p.lds_tile_offset);
     if constexpr (FOLD)
-      stream_block_fold<DT, NCMAX, KMAX>(p, sp, hsh, ssh, fs, dyn, wl, sh_go);
+      stream_block_fold<DT, NCMAX, KMAX>(p, sp, hsh, fs, dyn, wl, sh_go);
     else
-      stream_block<DT, NCMAX, KMAX>(p, sp, hsh, ssh, fs, dyn, wl, sh_go);
+      stream_block<DT, NCMAX, KMAX>(p, sp, hsh, fs, dyn, wl, sh_go);
     return;
   }
 
@@ -1715,16 +1682,12 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
     st.top_key[(size_t)req * p.N] = node_key(0.0f, 0, root, 0);
     st.top_node[(size_t)req * p.N] = 0;
   }
+  if (threadIdx.x == 0) ssh.abort = 0;
+  __syncthreads();
   for (int d = 0; d < p.B; ++d) {
     const int P = d == 0 ? 1 : p.kk;
-    if (threadIdx.x < 64) {
-      const int ok = wait_tags(p, d);
-      if (threadIdx.x == 0) sh_go = ok;
-    }
-    __syncthreads();
-    if (!sh_go) return;
-    sel_merge<KMAX>(p, d, p.R * P, ssh);
-    stage_select(p, st, d, P, 0, p.R, ssh, false);
+    if (!sel_merge<KMAX>(p, d, p.R * P, ssh)) return;
+    stage_select(p, st, d, P, 0, p.R, ssh, false, true);
   }
   for (int req = 0; req < p.R; ++req) emit_request(p, st, req);
 }
@@ -1766,7 +1729,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, i
       for (int i = 0; i < KMAX; ++i) other[i] = p.part_key[o * KMAX + i];
       list_merge(list, other);
       const SliceHead hd = p.part_hd[o];
-      lse_combine(m, s, hd.m, hd.s);
+      lse_combine(m, s, child_key_value(hd.key[0]), __uint_as_float((uint32_t)hd.sw));
     }
   }
 #pragma unroll
@@ -1797,7 +1760,28 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, i
     }
   }
   __syncthreads();
-  stage_select(p, global_state(p), d, P, req, 1, ssh, true);
+  stage_select(p, global_state(p), d, P, req, 1, ssh, true, false);
+}
+
+// Zero the words the persistent round polls (slice partials of every stage,
+// row and slice, and the frontier words) and mark every request as not built.
+__global__ __launch_bounds__(256) void clear_kernel(Plan p) {
+  const int per = p.kmax + kHeadKeys + 1;  // list words, then record words
+  const int nrec = p.stages * p.rows_max * p.G;
+  const int n = nrec * per;
+  const int stride = gridDim.x * blockDim.x;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const int rec = i / per, w = i - rec * per;
+    const int sr = rec / p.G, slice = rec - sr * p.G;  // (stage, row), slice
+    const size_t o = (size_t)sr * kSlicesMax + slice;
+    if (w < p.kmax)
+      p.part_key[o * p.kmax + w] = 0;
+    else
+      ((uint64_t*)(p.part_hd + o))[w - p.kmax] = 0;
+  }
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < p.stages * p.rows_max; i += stride)
+    p.front_w[i] = 0;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < p.R; i += stride) p.o_count[i] = -1;
 }
 
 __global__ __launch_bounds__(kEmitThreads) void emit_kernel(Plan p) {
@@ -1891,24 +1875,10 @@ StageFn select_fn(int kmax) {
   }
 }
 
-// Call tags of the persistent form: a 64-bit sequence started at a random
-// point, skipping 0 and all ones (fill patterns).  Stale tags in a reused
-// workspace come from other calls, so they never equal the current one; a
-// workspace that was never used by this process matches only by chance
-// (2^-64 per word).
-uint64_t next_epoch() {
-  static std::atomic<uint64_t> seq{[] {
-    std::random_device rd;
-    uint64_t x = ((uint64_t)rd() << 32) ^ rd() ^
-                 (uint64_t)std::chrono::high_resolution_clock::now().time_since_epoch().count();
-    x = (x ^ (x >> 30)) * 0xbf58476d1ce4e5b9ull;  // SplitMix64 output mix
-    x = (x ^ (x >> 27)) * 0x94d049bb133111ebull;
-    return x ^ (x >> 31);
-  }()};
-  for (;;) {
-    const uint64_t e = seq.fetch_add(1, std::memory_order_relaxed);
-    if (e != 0 && e != ~0ull) return e;
-  }
+// Call tags: 1 .. kTagMask in turn (0 is what the clear leaves).
+uint32_t next_tag() {
+  static std::atomic<uint32_t> seq{0};
+  return seq.fetch_add(1, std::memory_order_relaxed) % kTagMask + 1;
 }
 
 // Per-device facts for the persistent launch, queried once per device.
@@ -1981,9 +1951,15 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
         fit = 0;
     }
   }
+  p.tag = next_tag();
   if (narrow && fit > 0) {
     p.spin_ticks = 2 * di.ticks_per_s;  // a stage never legitimately waits 2 s
-    p.epoch = next_epoch();
+    // no word of an earlier use of the workspace may carry the call's tag
+    {
+      const int n = p.stages * p.rows_max * p.G * (p.kmax + kHeadKeys + 1) + p.stages * p.rows_max;
+      hipLaunchKernelGGL(clear_kernel, dim3(std::min((n + 255) / 256, 2048)), dim3(256), 0, st,
+                         p);
+    }
     void* args[] = {&p};
     const bool prof = profile_on();
     if (prof) profile_mark(st, "round_kernel");

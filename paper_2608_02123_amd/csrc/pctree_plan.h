@@ -21,11 +21,16 @@ constexpr int kFlagStride = 64;      // ints between two workgroups' flag words 
 
 // What a streaming workgroup publishes per (stage, row, slice) besides its
 // candidate list: the list's kHeadKeys best keys (0 past the list) and the
-// slice's (row max, sum of exp).
+// slice's sum of exp relative to its best logit (the logit of key[0]) in the
+// low half of `sw`.  Every published word carries the call's tag (the low
+// kTagBits of a key, the high half of `sw`), so that a reader can tell a
+// word of this call from a stale one without any ordering between words.
 constexpr int kHeadKeys = 3;
+constexpr int kTagBits = 10;
+constexpr uint32_t kTagMask = (1u << kTagBits) - 1;
 struct SliceHead {
   uint64_t key[kHeadKeys];
-  float m, s;
+  uint64_t sw;
 };
 static_assert(sizeof(SliceHead) == 32, "one SliceHead is two 16-byte loads");
 
@@ -72,10 +77,11 @@ struct Plan {
   uint64_t* top_key; // [R][N] running global top-N (sorted, descending)
   int* top_node;     // [R][N]
   uint64_t* part_key;// [stages][rows_max][kSlicesMax][kmax] per-slice candidate lists
-  SliceHead* part_hd;// [stages][rows_max][kSlicesMax] per-slice best key, (max, sum)
+  SliceHead* part_hd;// [stages][rows_max][kSlicesMax] per-slice best keys and sum
   int* req_bad;      // [R] root token outside [0, V)
-  uint64_t* tags;    // [stages][kSlicesMax]: call tag of each published slice partial
-  uint64_t epoch;    // this call's tag (unique per call; never 0 or all ones)
+  uint64_t* front_w; // [stages][rows_max] frontier of each stage (persistent form)
+  uint32_t tag;      // this call's tag, 1 .. kTagMask (published words carry it)
+  int pad_;
   long long spin_ticks;  // device wall-clock ticks a wait may last before aborting
   int lds_tiles;         // W tiles a streaming block keeps in LDS for the whole round
   int lds_top_offset;    // byte offset of the keeper's running top-N in the dynamic LDS
