@@ -135,7 +135,7 @@ size_t carve_workspace(Plan& p, char* base) {
   p.top_node = (int*)take(R * p.N * sizeof(int));
   const size_t parts = (size_t)p.stages * p.rows_max * kSlicesMax;
   p.part_key = (uint64_t*)take(parts * p.kmax * sizeof(uint64_t));
-  p.part_hd = (SliceHead*)take(parts * sizeof(SliceHead));
+  p.part_hd = (uint64_t*)take(parts * kRecWords * sizeof(uint64_t));
   p.req_bad = (int*)take(R * sizeof(int));
   p.front_w = (uint64_t*)take((size_t)p.stages * p.rows_max * sizeof(uint64_t));
   return off;

@@ -723,8 +723,14 @@ __device__ __forceinline__ void lds_pair_step(const Plan& p, const HeadLane& h, 
   tile_epilogue<DT, KMAX>(p, h, acc, l, t, ok && h.row_ok, r);
 }
 
+// Word 0 of slice 0 of the (stage, row) slice records; word w of slice s is
+// at + w * kSlicesMax + s.
+__device__ __forceinline__ uint64_t* slice_record(const Plan& p, int stage, int row) {
+  return p.part_hd + ((size_t)stage * p.rows_max + row) * kRecWords * kSlicesMax;
+}
+
 // Reduce the lanes' row states over the workgroup and publish the slice's
-// partial of every row (best keys and (max, sum)).
+// partial of every row (its list and its record).
 template <int KMAX, int WAVES, bool FOLD = false>
 __device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h, int stage,
                                                 int slice, RowAcc<KMAX>& r,
@@ -772,19 +778,20 @@ __device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h
 #pragma unroll
       for (int i = 0; i < KMAX; ++i)
         __hip_atomic_store(dst + i, r.list[i] | p.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      uint64_t* hd = (uint64_t*)(p.part_hd + o);
+      uint64_t* hd = slice_record(p, stage, h.row) + slice;
 #pragma unroll
       for (int i = 0; i < kHeadKeys; ++i)
-        __hip_atomic_store(hd + i, (i < KMAX ? r.list[i < KMAX ? i : 0] : 0ull) | p.tag,
+        __hip_atomic_store(hd + i * kSlicesMax, (i < KMAX ? r.list[i < KMAX ? i : 0] : 0ull) | p.tag,
                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       // the sum relative to the best logit (r.m is the logit of list[0])
       const uint64_t sw = ((uint64_t)p.tag << 32) | __float_as_uint(r.s);
-      __hip_atomic_store(hd + kHeadKeys, sw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(hd + kHeadKeys * kSlicesMax, sw, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
 
-// Published words of this call (see SliceHead).
+// Published words of this call (see kTagBits).
 __device__ __forceinline__ bool key_tagged(const Plan& p, uint64_t w) {
   return ((uint32_t)w & kTagMask) == p.tag;
 }
@@ -1181,6 +1188,15 @@ __device__ void stream_block_fold(const Plan& p, const Plan& sp,
 // Number of keys[0..n) greater than `key`; the loads of eight entries are
 // issued before any comparison (a dependent LDS read per entry would cost its
 // full latency n times).
+// A workgroup barrier for LDS traffic only: unlike __syncthreads() it does
+// not wait for the wave's outstanding global stores.
+__device__ __forceinline__ void lds_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 __device__ __forceinline__ int count_greater(const uint64_t* keys, int n, uint64_t key) {
   int cnt = 0;
   int c = 0;
@@ -1219,7 +1235,7 @@ __device__ void stage_select(const Plan& p, const State& st, int d, int P, int r
   const int nbase = d == 0 ? 1 : 1 + kk + (d - 1) * kk * kk;  // pool id of the first candidate
   const bool more = d + 1 < p.B;
 
-  int tok = 0;
+  int tok = 0, par = 0;
   float score = 0.0f;
   if (tid < ncand) {
     const int rq = tid / per_req;
@@ -1234,20 +1250,18 @@ __device__ void stage_select(const Plan& p, const State& st, int d, int P, int r
     tok = min(max(child_key_token(ck), 0), p.V - 1);
     const float lp = child_key_value(ck) - sh.lse[lrow];
     score = st.front_score[req * kk + pr] + lp;
-    const size_t id = (size_t)req * p.maxpool + nbase + ci;
-    p.node_tok[id] = tok;
-    p.node_par[id] = st.front_node[req * kk + pr];
-    p.node_depth[id] = d + 1;
-    p.node_score[id] = score;
+    par = st.front_node[req * kk + pr];
     sh.ckey[tid] = node_key(score, d + 1, tok, pr);
   }
-  __syncthreads();
+  // (the frontier's loads above have returned: LDS barriers suffice until
+  // the frontier is rewritten)
+  lds_barrier();
   // rank within the request's layer
   if (tid < ncand) {
     const int rq = tid / per_req;
     sh.rank[tid] = count_greater(sh.ckey + rq * per_req, per_req, sh.ckey[tid]);
   }
-  __syncthreads();
+  lds_barrier();
   // next frontier (every frontier slot was read above, before the barriers)
   if (more && tid < ncand && sh.rank[tid] < kk) {
     const int rq = tid / per_req;
@@ -1268,6 +1282,15 @@ __device__ void stage_select(const Plan& p, const State& st, int d, int P, int r
       p.t_pslot[o] = ci / kk;
       p.t_score[o] = score;
     }
+  }
+  // the pool entries of the stage's candidates
+  if (tid < ncand) {
+    const int rq = tid / per_req;
+    const size_t id = (size_t)(req0 + rq) * p.maxpool + nbase + (tid - rq * per_req);
+    p.node_tok[id] = tok;
+    p.node_par[id] = par;
+    p.node_depth[id] = d + 1;
+    p.node_score[id] = score;
   }
   // running global top-N, one request at a time: every element's new
   // position is its rank in the union (both sides are sorted), computed
@@ -1326,6 +1349,7 @@ __device__ __forceinline__ bool sel_merge_rows(const Plan& p, int d, int rows, S
   bool alive = true;
   for (int row = wave; row < rows && alive; row += nwave) {
     const size_t base = ((size_t)d * p.rows_max + row) * kSlicesMax;
+    const uint64_t* recs = slice_record(p, d, row);
     uint64_t hk[HPL][HK], first[HPL];
     float hs[HPL];
     bool have[HPL];
@@ -1341,10 +1365,10 @@ __device__ __forceinline__ bool sel_merge_rows(const Plan& p, int d, int rows, S
 #pragma unroll
       for (int c = 0; c < HPL; ++c) {
         if (!have[c]) {
-          const uint64_t* rec = (const uint64_t*)(p.part_hd + base + lane + 64 * c);
-          uint64_t w[kHeadKeys + 1];
+          const uint64_t* rec = recs + lane + 64 * c;
+          uint64_t w[kRecWords];
 #pragma unroll
-          for (int i = 0; i <= kHeadKeys; ++i) w[i] = load_agent(rec + i);
+          for (int i = 0; i < kRecWords; ++i) w[i] = load_agent(rec + i * kSlicesMax);
           bool ok = sum_tagged(p, w[kHeadKeys]);
 #pragma unroll
           for (int i = 0; i < kHeadKeys; ++i) ok = ok && key_tagged(p, w[i]);
@@ -1728,8 +1752,9 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, i
 #pragma unroll
       for (int i = 0; i < KMAX; ++i) other[i] = p.part_key[o * KMAX + i];
       list_merge(list, other);
-      const SliceHead hd = p.part_hd[o];
-      lse_combine(m, s, child_key_value(hd.key[0]), __uint_as_float((uint32_t)hd.sw));
+      const uint64_t* rec = slice_record(p, 0, grow) + g;
+      lse_combine(m, s, child_key_value(rec[0]),
+                  __uint_as_float((uint32_t)rec[kHeadKeys * kSlicesMax]));
     }
   }
 #pragma unroll
@@ -1766,18 +1791,17 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, i
 // Zero the words the persistent round polls (slice partials of every stage,
 // row and slice, and the frontier words) and mark every request as not built.
 __global__ __launch_bounds__(256) void clear_kernel(Plan p) {
-  const int per = p.kmax + kHeadKeys + 1;  // list words, then record words
+  const int per = p.kmax + kRecWords;  // list words, then record words
   const int nrec = p.stages * p.rows_max * p.G;
   const int n = nrec * per;
   const int stride = gridDim.x * blockDim.x;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
     const int rec = i / per, w = i - rec * per;
     const int sr = rec / p.G, slice = rec - sr * p.G;  // (stage, row), slice
-    const size_t o = (size_t)sr * kSlicesMax + slice;
     if (w < p.kmax)
-      p.part_key[o * p.kmax + w] = 0;
+      p.part_key[((size_t)sr * kSlicesMax + slice) * p.kmax + w] = 0;
     else
-      ((uint64_t*)(p.part_hd + o))[w - p.kmax] = 0;
+      p.part_hd[((size_t)sr * kRecWords + (w - p.kmax)) * kSlicesMax + slice] = 0;
   }
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < p.stages * p.rows_max; i += stride)
     p.front_w[i] = 0;
@@ -1956,7 +1980,7 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
     p.spin_ticks = 2 * di.ticks_per_s;  // a stage never legitimately waits 2 s
     // no word of an earlier use of the workspace may carry the call's tag
     {
-      const int n = p.stages * p.rows_max * p.G * (p.kmax + kHeadKeys + 1) + p.stages * p.rows_max;
+      const int n = p.stages * p.rows_max * p.G * (p.kmax + kRecWords) + p.stages * p.rows_max;
       hipLaunchKernelGGL(clear_kernel, dim3(std::min((n + 255) / 256, 2048)), dim3(256), 0, st,
                          p);
     }

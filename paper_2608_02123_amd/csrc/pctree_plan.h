@@ -20,19 +20,18 @@ constexpr int kNarrowRows = 16;      // frontier rows (R * k') one column block 
 constexpr int kFlagStride = 64;      // ints between two workgroups' flag words (256 B)
 
 // What a streaming workgroup publishes per (stage, row, slice) besides its
-// candidate list: the list's kHeadKeys best keys (0 past the list) and the
-// slice's sum of exp relative to its best logit (the logit of key[0]) in the
-// low half of `sw`.  Every published word carries the call's tag (the low
-// kTagBits of a key, the high half of `sw`), so that a reader can tell a
-// word of this call from a stale one without any ordering between words.
+// candidate list, the slice record: kRecWords 64-bit words, the list's
+// kHeadKeys best keys (0 past the list) and the slice's sum of exp relative to
+// its best logit (the logit of the first key) in the low half of the last
+// word.  Records are stored word-major, [stage][row][word][slice], so that a
+// wave reads one word of 64 slices as 512 contiguous bytes.  Every published
+// word carries the call's tag (the low kTagBits of a key, the high half of the
+// sum word), so that a reader can tell a word of this call from a stale one
+// without any ordering between words.
 constexpr int kHeadKeys = 3;
+constexpr int kRecWords = kHeadKeys + 1;
 constexpr int kTagBits = 10;
 constexpr uint32_t kTagMask = (1u << kTagBits) - 1;
-struct SliceHead {
-  uint64_t key[kHeadKeys];
-  uint64_t sw;
-};
-static_assert(sizeof(SliceHead) == 32, "one SliceHead is two 16-byte loads");
 
 // Everything one round needs, passed by value to every kernel.
 struct Plan {
@@ -77,7 +76,7 @@ struct Plan {
   uint64_t* top_key; // [R][N] running global top-N (sorted, descending)
   int* top_node;     // [R][N]
   uint64_t* part_key;// [stages][rows_max][kSlicesMax][kmax] per-slice candidate lists
-  SliceHead* part_hd;// [stages][rows_max][kSlicesMax] per-slice best keys and sum
+  uint64_t* part_hd; // [stages][rows_max][kRecWords][kSlicesMax] slice records
   int* req_bad;      // [R] root token outside [0, V)
   uint64_t* front_w; // [stages][rows_max] frontier of each stage (persistent form)
   uint32_t tag;      // this call's tag, 1 .. kTagMask (published words carry it)
