@@ -496,6 +496,7 @@ __global__ __launch_bounds__(kEmitThreads) void prologue_kernel(Plan p) {
 template <int KMAX, int WAVES>
 struct HeadShared {
   uint64_t wl[WAVES][kTile][KMAX];
+  uint64_t wt[WAVES][kTile][KMAX < 4 ? KMAX : 4];
   float2 wms[WAVES][kTile];
 };
 
@@ -730,63 +731,112 @@ __device__ __forceinline__ uint64_t* slice_record(const Plan& p, int stage, int 
 }
 
 // Reduce the lanes' row states over the workgroup and publish the slice's
-// partial of every row (its list and its record).
+// partial of every row.  Two reduction trees: the first carries only the
+// lanes' best four keys and the (max, sum) pairs and ends in the record, which
+// is all the keeper needs unless a row's record keys do not settle it; the
+// second then carries the full lists, which only that rare case reads.
+// Rows live in lanes col, col+16, col+32, col+48 of every wave (and, folded,
+// in lanes col and col ^ 8).
 template <int KMAX, int WAVES, bool FOLD = false>
 __device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h, int stage,
                                                 int slice, RowAcc<KMAX>& r,
                                                 HeadShared<KMAX, WAVES>& sh) {
-  if constexpr (FOLD) {  // the two lanes of a folded row: col and col ^ 8 (DPP row_ror:8)
-    uint64_t o[KMAX];
+  constexpr int HT = KMAX < 4 ? KMAX : 4;
+  const size_t o = ((size_t)stage * p.rows_max + h.row) * kSlicesMax + slice;
+  const bool writer = h.grp == 0 && h.row_ok && h.lead;
+  {
+    uint64_t t[HT];
 #pragma unroll
-    for (int i = 0; i < KMAX; ++i) o[i] = dpp64<0x128, 0xF>(r.list[i]);
-    list_merge(r.list, o);
-    lse_combine(r.m, r.s, dppf<0x128, 0xF>(r.m, kNegBig), dppf<0x128, 0xF>(r.s, 0.0f));
+    for (int i = 0; i < HT; ++i) t[i] = r.list[i];
+    float m = r.m, sum = r.s;
+    if constexpr (FOLD) {
+      uint64_t x[HT];
+#pragma unroll
+      for (int i = 0; i < HT; ++i) x[i] = dpp64<0x128, 0xF>(t[i]);
+      list_merge(t, x);
+      lse_combine(m, sum, dppf<0x128, 0xF>(m, kNegBig), dppf<0x128, 0xF>(sum, 0.0f));
+    }
+    list_merge_pair<16>(t);
+    lse_combine_pair<16>(m, sum);
+    list_merge_pair<32>(t);
+    lse_combine_pair<32>(m, sum);
+    if (h.grp == 0) {
+#pragma unroll
+      for (int i = 0; i < HT; ++i) sh.wt[h.wave][h.col][i] = t[i];
+      sh.wms[h.wave][h.col] = make_float2(m, sum);
+    }
+    __syncthreads();
+    if (h.wave == 0) {
+#pragma unroll
+      for (int i = 0; i < HT; ++i) t[i] = sh.wt[h.grp][h.col][i];
+      m = sh.wms[h.grp][h.col].x;
+      sum = sh.wms[h.grp][h.col].y;
+#pragma unroll
+      for (int w = h.grp + 4; w < WAVES; w += 4) {
+        uint64_t x[HT];
+#pragma unroll
+        for (int i = 0; i < HT; ++i) x[i] = sh.wt[w][h.col][i];
+        list_merge(t, x);
+        lse_combine(m, sum, sh.wms[w][h.col].x, sh.wms[w][h.col].y);
+      }
+      list_merge_pair<16>(t);
+      lse_combine_pair<16>(m, sum);
+      list_merge_pair<32>(t);
+      lse_combine_pair<32>(m, sum);
+      if (writer) {
+        // tagged words, stored write-through at agent scope: each one is
+        // valid on its own once it lands (keys have their low kTagBits clear)
+        uint64_t* hd = slice_record(p, stage, h.row) + slice;
+#pragma unroll
+        for (int i = 0; i < kHeadKeys; ++i)
+          __hip_atomic_store(hd + i * kSlicesMax, (i < HT ? t[i < HT ? i : 0] : 0ull) | p.tag,
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // the sum relative to the best logit (m is the logit of t[0])
+        __hip_atomic_store(hd + kHeadKeys * kSlicesMax,
+                           ((uint64_t)p.tag << 32) | __float_as_uint(sum), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+        if constexpr (HT == KMAX) {
+          uint64_t* dst = p.part_key + o * KMAX;
+#pragma unroll
+          for (int i = 0; i < KMAX; ++i)
+            __hip_atomic_store(dst + i, t[i] | p.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    }
   }
-  // rows live in lanes col, col+16, col+32, col+48 of every wave
-  list_merge_pair<16>(r.list);
-  lse_combine_pair<16>(r.m, r.s);
-  list_merge_pair<32>(r.list);
-  lse_combine_pair<32>(r.m, r.s);
-  if (h.grp == 0) {
+  if constexpr (HT < KMAX) {
+    if constexpr (FOLD) {
+      uint64_t x[KMAX];
 #pragma unroll
-    for (int i = 0; i < KMAX; ++i) sh.wl[h.wave][h.col][i] = r.list[i];
-    sh.wms[h.wave][h.col] = make_float2(r.m, r.s);
-  }
-  __syncthreads();
-  if (h.wave == 0) {
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) r.list[i] = sh.wl[h.grp][h.col][i];
-    r.m = sh.wms[h.grp][h.col].x;
-    r.s = sh.wms[h.grp][h.col].y;
-#pragma unroll
-    for (int w = h.grp + 4; w < WAVES; w += 4) {
-      uint64_t o[KMAX];
-#pragma unroll
-      for (int i = 0; i < KMAX; ++i) o[i] = sh.wl[w][h.col][i];
-      list_merge(r.list, o);
-      lse_combine(r.m, r.s, sh.wms[w][h.col].x, sh.wms[w][h.col].y);
+      for (int i = 0; i < KMAX; ++i) x[i] = dpp64<0x128, 0xF>(r.list[i]);
+      list_merge(r.list, x);
     }
     list_merge_pair<16>(r.list);
-    lse_combine_pair<16>(r.m, r.s);
     list_merge_pair<32>(r.list);
-    lse_combine_pair<32>(r.m, r.s);
-    if (h.grp == 0 && h.row_ok && h.lead) {
-      // tagged words, stored write-through at agent scope: each one is
-      // valid on its own once it lands (keys have their low kTagBits clear)
-      const size_t o = ((size_t)stage * p.rows_max + h.row) * kSlicesMax + slice;
-      uint64_t* dst = p.part_key + o * KMAX;
+    if (h.grp == 0) {
 #pragma unroll
-      for (int i = 0; i < KMAX; ++i)
-        __hip_atomic_store(dst + i, r.list[i] | p.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      uint64_t* hd = slice_record(p, stage, h.row) + slice;
+      for (int i = 0; i < KMAX; ++i) sh.wl[h.wave][h.col][i] = r.list[i];
+    }
+    __syncthreads();
+    if (h.wave == 0) {
 #pragma unroll
-      for (int i = 0; i < kHeadKeys; ++i)
-        __hip_atomic_store(hd + i * kSlicesMax, (i < KMAX ? r.list[i < KMAX ? i : 0] : 0ull) | p.tag,
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      // the sum relative to the best logit (r.m is the logit of list[0])
-      const uint64_t sw = ((uint64_t)p.tag << 32) | __float_as_uint(r.s);
-      __hip_atomic_store(hd + kHeadKeys * kSlicesMax, sw, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
+      for (int i = 0; i < KMAX; ++i) r.list[i] = sh.wl[h.grp][h.col][i];
+#pragma unroll
+      for (int w = h.grp + 4; w < WAVES; w += 4) {
+        uint64_t x[KMAX];
+#pragma unroll
+        for (int i = 0; i < KMAX; ++i) x[i] = sh.wl[w][h.col][i];
+        list_merge(r.list, x);
+      }
+      list_merge_pair<16>(r.list);
+      list_merge_pair<32>(r.list);
+      if (writer) {
+        uint64_t* dst = p.part_key + o * KMAX;
+#pragma unroll
+        for (int i = 0; i < KMAX; ++i)
+          __hip_atomic_store(dst + i, r.list[i] | p.tag, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
   }
 }
@@ -1185,9 +1235,6 @@ __device__ void stream_block_fold(const Plan& p, const Plan& sp,
 // ---------------------------------------------------------------------------
 // stage selection on merged rows (shared by both launch forms)
 // ---------------------------------------------------------------------------
-// Number of keys[0..n) greater than `key`; the loads of eight entries are
-// issued before any comparison (a dependent LDS read per entry would cost its
-// full latency n times).
 // A workgroup barrier for LDS traffic only: unlike __syncthreads() it does
 // not wait for the wave's outstanding global stores.
 __device__ __forceinline__ void lds_barrier() {
@@ -1197,9 +1244,19 @@ __device__ __forceinline__ void lds_barrier() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+// Number of keys[0..n) greater than `key`; the loads of up to 32 entries are
+// issued before any comparison (a dependent LDS read per entry, or per small
+// batch, would cost its full latency over and over).
 __device__ __forceinline__ int count_greater(const uint64_t* keys, int n, uint64_t key) {
   int cnt = 0;
   int c = 0;
+  for (; c + 32 <= n; c += 32) {
+    uint64_t v[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) v[i] = keys[c + i];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) cnt += v[i] > key;
+  }
   for (; c + 8 <= n; c += 8) {
     uint64_t v[8];
 #pragma unroll
