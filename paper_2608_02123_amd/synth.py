@@ -31,7 +31,8 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-__all__ = ["Workload", "CONFIGS", "make_inputs", "round_to_bf16", "bf16_bits"]
+__all__ = ["Workload", "CONFIGS", "make_inputs", "round_to_bf16", "bf16_bits",
+           "random_tree", "target_next", "make_kv_cache"]
 
 
 @dataclass(frozen=True)
@@ -158,3 +159,67 @@ def make_inputs(w: Workload) -> dict:
         "prefix_len": prefix_len,
         "workload": w,
     }
+
+
+# ---------------------------------------------------------------------------
+# Inputs of the verification bookkeeping after a round
+# ---------------------------------------------------------------------------
+
+def random_tree(rng: np.random.Generator, N: int, count: int, max_depth: int, V: int):
+    """A random tree of ``count`` nodes in ``N`` slots, shaped like an emitted one.
+
+    Node 0 is the root; node i > 0 hangs below a uniformly drawn earlier node
+    of depth < ``max_depth`` (so ``parent[i] < i``), with a token drawn
+    uniformly from the vocabulary and distinct from its siblings' tokens.
+    Slots past ``count`` hold -1.  Returns ``(token, parent, depth)`` int32.
+    """
+    token = np.full(N, -1, np.int32)
+    parent = np.full(N, -1, np.int32)
+    depth = np.full(N, -1, np.int32)
+    if count <= 0:
+        return token, parent, depth
+    token[0] = rng.integers(0, V)
+    depth[0] = 0
+    kids: dict[int, set] = {0: set()}
+    for i in range(1, count):
+        open_nodes = [j for j in range(i) if depth[j] < max_depth and len(kids[j]) < V]
+        p = int(open_nodes[rng.integers(0, len(open_nodes))])
+        t = int(rng.integers(0, V))
+        while t in kids[p]:
+            t = int(rng.integers(0, V))
+        kids[p].add(t)
+        kids[i] = set()
+        token[i], parent[i], depth[i] = t, p, depth[p] + 1
+    return token, parent, depth
+
+
+def target_next(rng: np.random.Generator, token: np.ndarray, parent: np.ndarray, count: int,
+                V: int, accept_p: float) -> np.ndarray:
+    """Synthetic greedy predictions of the target at each tree node.
+
+    Stands in for the argmax of the verification forward's logits: at a node
+    with children, with probability ``accept_p`` the prediction is the token
+    of one of its children (drawn uniformly), otherwise a uniform token.
+    """
+    N = len(token)
+    out = rng.integers(0, V, size=N).astype(np.int32)
+    children: dict[int, list] = {}
+    for i in range(1, max(0, min(count, N))):
+        children.setdefault(int(parent[i]), []).append(int(token[i]))
+    for i in range(max(0, min(count, N))):
+        kids = children.get(i)
+        if kids and rng.random() < accept_p:
+            out[i] = kids[int(rng.integers(0, len(kids)))]
+    return out
+
+
+def make_kv_cache(rng: np.random.Generator, groups: int, capacity: int, width: int) -> np.ndarray:
+    """A synthetic bf16 KV cache ``[groups][capacity][width]`` (as uint16 bits).
+
+    ``groups`` stands for (layer, K or V) pairs of a target model; every slot
+    holds ``width`` bf16 values (heads x head dimension).  Random bit patterns
+    of finite values: the compaction only moves them.
+    """
+    bits = rng.integers(0, 1 << 16, size=(groups, capacity, width), dtype=np.uint32)
+    bits &= ~np.uint32(0x4000)  # exponent below all ones: finite values
+    return bits.astype(np.uint16)
