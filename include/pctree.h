@@ -151,6 +151,62 @@ pctree_status pctree_chain_decode(const pctree_shape* shape, const pctree_inputs
                                   int32_t* chain_token, float* chain_logprob, void* workspace,
                                   size_t workspace_bytes, void* stream);
 
+/* ---------------------------------------------------------------------
+ * Verification bookkeeping after a round (Sec. 4.2; App. A, "Tensor
+ * implementation").  The emitted tree goes through one target forward, which
+ * predicts a greedy next token at every node; these calls turn that into the
+ * accepted draft and compact the per-node cache entries.  Same conventions as
+ * above (device pointers, asynchronous on `stream`, host-side checks only).
+ * W = max_depth + 1 is the width of a row; max_depth is normally B.
+ * --------------------------------------------------------------------- */
+
+/* Retrieve indices (App. A): one padded root-to-leaf row per leaf.
+ * parent [R][N], count [R] as emitted by pctree_build_tree.  A leaf is a node
+ * i < count that is no node's parent; leaf q in ascending node order gets row
+ * q of rows [R][N][W]: the node indices from the root down to the leaf,
+ * padded with -1.  nrows [R] = number of leaves; rows past it are all -1.
+ * Malformed trees do not fault: a parent index outside [0, i) ends the
+ * upward walk from node i (that node then heads its row), and a path longer
+ * than W keeps its first W nodes from the head.
+ * Limits: N <= PCTREE_MAX_MASK_BUDGET, max_depth <= PCTREE_MAX_BLOCK. */
+pctree_status pctree_build_retrieve(const int32_t* parent, const int32_t* count, int32_t requests,
+                                    int32_t budget, int32_t max_depth, int32_t* rows,
+                                    int32_t* nrows, void* stream);
+
+/* Greedy tree acceptance (Sec. 4.2: the standard greedy tree rule; App. A).
+ * token [R][N] draft tokens; rows [R][N][W] and nrows [R] from
+ * pctree_build_retrieve; target_next [R][N] the target's greedy next token
+ * after each node.  Along a row, position l >= 1 is accepted while
+ * token[row[l]] == target_next[row[l-1]]; the row accepting the most
+ * positions wins (the lowest row on ties).  Outputs per request:
+ * accept_len [R] accepted draft tokens (root excluded), accept_row [R] the
+ * winning row (-1 if there is none), accept_node [R][W] its accepted node
+ * indices from the root, padded with -1, and bonus [R] = target_next at the
+ * last accepted node (-1 if there is no row).  A row entry outside [0, N)
+ * ends that row.  Limits as for pctree_build_retrieve. */
+pctree_status pctree_accept_greedy(const int32_t* token, const int32_t* rows,
+                                   const int32_t* nrows, const int32_t* target_next,
+                                   int32_t requests, int32_t budget, int32_t max_depth,
+                                   int32_t* accept_len, int32_t* accept_row,
+                                   int32_t* accept_node, int32_t* bonus, void* stream);
+
+/* Compaction after acceptance (App. A): the cache entries of the accepted
+ * row move right after the verified prefix.  `cache` holds, per request and
+ * group (e.g. one layer's K or V, or the target hidden states), `capacity`
+ * slots of slot_bytes each, contiguous: slot s of group g of request r starts
+ * at cache + r*request_stride + g*group_stride + s*slot_bytes.  Tree node i
+ * sits at slot prefix_len[r] + i; the accepted nodes n_0..n_a
+ * (accept_node [R][W], accept_len [R] from pctree_accept_greedy) move, in
+ * place, to slots prefix_len[r] + 0..a.  Other slots keep their contents.
+ * A request whose accepted nodes are not strictly increasing, not below N,
+ * or reach past `capacity` is left untouched.  slot_bytes, both strides and
+ * `cache` must be multiples of 16. */
+pctree_status pctree_compact_kv(void* cache, int64_t request_stride, int64_t group_stride,
+                                int32_t groups, int32_t capacity, int32_t slot_bytes,
+                                const int32_t* prefix_len, const int32_t* accept_node,
+                                const int32_t* accept_len, int32_t requests, int32_t budget,
+                                int32_t max_depth, void* stream);
+
 /* Static, human-readable name of a status code. */
 const char* pctree_status_string(pctree_status status);
 

@@ -11,7 +11,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libpctree.so")
-SOURCES = ["pctree_api.hip", "pctree_kernels.hip", "pctree_profile.hip"]
+SOURCES = ["pctree_api.hip", "pctree_kernels.hip", "pctree_profile.hip", "pctree_verify.hip"]
 ARCH = "gfx950"
 
 
@@ -38,14 +38,17 @@ def compile_flags() -> list[str]:
 def build(verbose: bool = False) -> str:
     """Compile every HIP source for gfx950 and link ``libpctree.so``; returns its path."""
     cc = hipcc()
-    objs = []
-    for src in SOURCES:
+    objs, procs = [], []
+    for src in SOURCES:  # the sources compile side by side
         obj = os.path.join(CSRC, src.replace(".hip", ".o"))
         cmd = [cc, *compile_flags(), "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
-        subprocess.run(cmd, check=True, stderr=None if verbose else subprocess.DEVNULL)
+        procs.append((cmd, subprocess.Popen(cmd, stderr=None if verbose else subprocess.DEVNULL)))
         objs.append(obj)
+    for cmd, proc in procs:
+        if proc.wait() != 0:
+            raise subprocess.CalledProcessError(proc.returncode, cmd)
     tmp = LIB + ".tmp"
     cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:

@@ -6,6 +6,7 @@
 #include <algorithm>
 
 #include "pctree_plan.h"
+#include "pctree_verify.h"
 
 namespace pctree {
 
@@ -243,6 +244,78 @@ pctree_status pctree_chain_decode(const pctree_shape* shape, const pctree_inputs
     p.t_pslot = nullptr;
     p.t_score = nullptr;
     return enqueue(p, stream);
+  } catch (...) {
+    return PCTREE_ERR_HIP;
+  }
+}
+
+pctree_status pctree_build_retrieve(const int32_t* parent, const int32_t* count, int32_t requests,
+                                    int32_t budget, int32_t max_depth, int32_t* rows,
+                                    int32_t* nrows, void* stream) {
+  try {
+    if (!parent || !count || !rows || !nrows || requests < 1 || budget < 1 || max_depth < 0)
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    if (!aligned(parent, 4) || !aligned(count, 4) || !aligned(rows, 4) || !aligned(nrows, 4))
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    if (budget > PCTREE_MAX_MASK_BUDGET || max_depth > PCTREE_MAX_BLOCK || requests > 65535)
+      return PCTREE_ERR_UNSUPPORTED;
+    (void)hipGetLastError();
+    const hipError_t e = launch_retrieve(parent, count, requests, budget, max_depth + 1, rows,
+                                         nrows, (hipStream_t)stream);
+    return e == hipSuccess ? PCTREE_OK : PCTREE_ERR_HIP;
+  } catch (...) {
+    return PCTREE_ERR_HIP;
+  }
+}
+
+pctree_status pctree_accept_greedy(const int32_t* token, const int32_t* rows,
+                                   const int32_t* nrows, const int32_t* target_next,
+                                   int32_t requests, int32_t budget, int32_t max_depth,
+                                   int32_t* accept_len, int32_t* accept_row,
+                                   int32_t* accept_node, int32_t* bonus, void* stream) {
+  try {
+    if (!token || !rows || !nrows || !target_next || !accept_len || !accept_row ||
+        !accept_node || !bonus || requests < 1 || budget < 1 || max_depth < 0)
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    for (const void* q : {(const void*)token, (const void*)rows, (const void*)nrows,
+                          (const void*)target_next, (const void*)accept_len,
+                          (const void*)accept_row, (const void*)accept_node, (const void*)bonus})
+      if (!aligned(q, 4)) return PCTREE_ERR_INVALID_ARGUMENT;
+    if (budget > PCTREE_MAX_MASK_BUDGET || max_depth > PCTREE_MAX_BLOCK || requests > 65535)
+      return PCTREE_ERR_UNSUPPORTED;
+    (void)hipGetLastError();
+    const hipError_t e = launch_accept(token, rows, nrows, target_next, requests, budget,
+                                       max_depth + 1, accept_len, accept_row, accept_node, bonus,
+                                       (hipStream_t)stream);
+    return e == hipSuccess ? PCTREE_OK : PCTREE_ERR_HIP;
+  } catch (...) {
+    return PCTREE_ERR_HIP;
+  }
+}
+
+pctree_status pctree_compact_kv(void* cache, int64_t request_stride, int64_t group_stride,
+                                int32_t groups, int32_t capacity, int32_t slot_bytes,
+                                const int32_t* prefix_len, const int32_t* accept_node,
+                                const int32_t* accept_len, int32_t requests, int32_t budget,
+                                int32_t max_depth, void* stream) {
+  try {
+    if (!cache || !prefix_len || !accept_node || !accept_len || requests < 1 || budget < 1 ||
+        max_depth < 0 || groups < 1 || capacity < 1 || slot_bytes < 16)
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    if (!aligned(cache, 16) || slot_bytes % 16 != 0 || request_stride % 16 != 0 ||
+        group_stride % 16 != 0 || request_stride < 0 || group_stride < 0 ||
+        !aligned(prefix_len, 4) || !aligned(accept_node, 4) || !aligned(accept_len, 4))
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    if (max_depth > PCTREE_MAX_BLOCK || requests > 65535 || budget > PCTREE_MAX_MASK_BUDGET)
+      return PCTREE_ERR_UNSUPPORTED;
+    // the grid covers groups x (slot_bytes / 16) columns per request
+    if ((long long)groups * (slot_bytes / 16) > (long long)INT32_MAX)
+      return PCTREE_ERR_UNSUPPORTED;
+    (void)hipGetLastError();
+    const hipError_t e = launch_compact(cache, request_stride, group_stride, groups, capacity,
+                                        slot_bytes, prefix_len, accept_node, accept_len, requests,
+                                        budget, max_depth + 1, (hipStream_t)stream);
+    return e == hipSuccess ? PCTREE_OK : PCTREE_ERR_HIP;
   } catch (...) {
     return PCTREE_ERR_HIP;
   }

@@ -19,6 +19,9 @@ __all__ = [
     "build_tree",
     "build_mask",
     "chain_decode",
+    "build_retrieve",
+    "accept_greedy",
+    "compact_kv",
     "TreeBuilder",
     "status_string",
     "F32",
@@ -80,6 +83,14 @@ def lib() -> ctypes.CDLL:
         L.pctree_chain_decode.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(_Inputs), vp, vp,
                                           vp, sz, vp]
         L.pctree_chain_decode.restype = ctypes.c_int
+        i32, i64 = ctypes.c_int32, ctypes.c_int64
+        L.pctree_build_retrieve.argtypes = [vp, vp, i32, i32, i32, vp, vp, vp]
+        L.pctree_build_retrieve.restype = ctypes.c_int
+        L.pctree_accept_greedy.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp]
+        L.pctree_accept_greedy.restype = ctypes.c_int
+        L.pctree_compact_kv.argtypes = [vp, i64, i64, i32, i32, i32, vp, vp, vp, i32, i32, i32,
+                                        vp]
+        L.pctree_compact_kv.restype = ctypes.c_int
         L.pctree_status_string.argtypes = [ctypes.c_int]
         L.pctree_status_string.restype = ctypes.c_char_p
         L.pctree_abi_version.argtypes = []
@@ -248,6 +259,64 @@ def chain_decode(L, E, Wt, h, root, prefix_len=None, stream=None):
                                    ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream))
     _check(st, "pctree_chain_decode")
     return toks, lps
+
+
+def _int32_dev(name, t):
+    if t.dtype != torch.int32 or not t.is_cuda or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous int32 device tensor")
+
+
+def build_retrieve(parent, count, max_depth, stream=None):
+    """Retrieve rows of emitted trees: (rows [R][N][max_depth+1], nrows [R]) int32."""
+    _int32_dev("parent", parent)
+    _int32_dev("count", count)
+    R, N = parent.shape
+    rows = torch.empty(R, N, max_depth + 1, dtype=torch.int32, device=parent.device)
+    nrows = torch.empty(R, dtype=torch.int32, device=parent.device)
+    st = lib().pctree_build_retrieve(_ptr(parent), _ptr(count), R, N, max_depth, _ptr(rows),
+                                     _ptr(nrows), _stream(stream))
+    _check(st, "pctree_build_retrieve")
+    return rows, nrows
+
+
+def accept_greedy(token, rows, nrows, target_next, stream=None):
+    """Greedy tree acceptance over retrieve rows; returns a dict of int32 tensors
+    ``accept_len [R]``, ``accept_row [R]``, ``accept_node [R][W]``, ``bonus [R]``."""
+    for name, t in (("token", token), ("rows", rows), ("nrows", nrows),
+                    ("target_next", target_next)):
+        _int32_dev(name, t)
+    R, N, W = rows.shape
+    if tuple(token.shape) != (R, N) or tuple(target_next.shape) != (R, N):
+        raise ValueError("token and target_next must be [R][N] like the rows")
+    i32 = dict(dtype=torch.int32, device=rows.device)
+    out = {"accept_len": torch.empty(R, **i32), "accept_row": torch.empty(R, **i32),
+           "accept_node": torch.empty(R, W, **i32), "bonus": torch.empty(R, **i32)}
+    st = lib().pctree_accept_greedy(_ptr(token), _ptr(rows), _ptr(nrows), _ptr(target_next), R, N,
+                                    W - 1, _ptr(out["accept_len"]), _ptr(out["accept_row"]),
+                                    _ptr(out["accept_node"]), _ptr(out["bonus"]), _stream(stream))
+    _check(st, "pctree_accept_greedy")
+    return out
+
+
+def compact_kv(cache, prefix_len, accept_node, accept_len, budget, stream=None):
+    """Move each request's accepted cache slots right after its prefix, in place.
+
+    ``cache [R][groups][capacity][...]`` is any contiguous device tensor whose
+    trailing dimensions form one slot (a multiple of 16 bytes).
+    """
+    if not cache.is_cuda or not cache.is_contiguous() or cache.dim() < 3:
+        raise ValueError("cache must be a contiguous [R][groups][capacity][...] device tensor")
+    for name, t in (("prefix_len", prefix_len), ("accept_node", accept_node),
+                    ("accept_len", accept_len)):
+        _int32_dev(name, t)
+    R, G, T = cache.shape[:3]
+    es = cache.element_size()
+    slot = cache[0, 0, 0].numel() * es
+    st = lib().pctree_compact_kv(_ptr(cache), cache.stride(0) * es, cache.stride(1) * es, G, T,
+                                 slot, _ptr(prefix_len), _ptr(accept_node), _ptr(accept_len), R,
+                                 budget, accept_node.shape[1] - 1, _stream(stream))
+    _check(st, "pctree_compact_kv")
+    return cache
 
 
 def device_inputs(inp: dict, device="cuda") -> dict:

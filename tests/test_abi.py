@@ -152,3 +152,51 @@ def test_chain_decode_validation():
              None) == P.ERR_WORKSPACE
     assert f(ctypes.byref(s), None, vp(A), vp(A), vp(A * 16), 1 << 30,
              None) == P.ERR_INVALID_ARGUMENT
+
+
+def test_build_retrieve_validation():
+    f = P.lib().pctree_build_retrieve
+    assert f(None, A, 1, 8, 4, A, A, None) == P.ERR_INVALID_ARGUMENT
+    assert f(A, A, 0, 8, 4, A, A, None) == P.ERR_INVALID_ARGUMENT
+    assert f(A, A, 1, 0, 4, A, A, None) == P.ERR_INVALID_ARGUMENT
+    assert f(A, A, 1, 8, -1, A, A, None) == P.ERR_INVALID_ARGUMENT
+    assert f(A, A, 1, 8, 4, None, A, None) == P.ERR_INVALID_ARGUMENT
+    assert f(A, A + 2, 1, 8, 4, A, A, None) == P.ERR_INVALID_ARGUMENT
+    assert f(A, A, 1, 1025, 4, A, A, None) == P.ERR_UNSUPPORTED
+    assert f(A, A, 1, 8, 64, A, A, None) == P.ERR_UNSUPPORTED
+
+
+def test_accept_greedy_validation():
+    f = P.lib().pctree_accept_greedy
+    ok = [A, A, A, A, 1, 8, 4, A, A, A, A]
+    for i in (0, 1, 2, 3, 7, 8, 9, 10):
+        args = list(ok)
+        args[i] = None
+        assert f(*args, None) == P.ERR_INVALID_ARGUMENT, i
+        args[i] = A + 2
+        assert f(*args, None) == P.ERR_INVALID_ARGUMENT, i
+    for i, bad in ((4, 0), (5, 0), (6, -1)):
+        args = list(ok)
+        args[i] = bad
+        assert f(*args, None) == P.ERR_INVALID_ARGUMENT, i
+    for i, big in ((5, 1025), (6, 64)):
+        args = list(ok)
+        args[i] = big
+        assert f(*args, None) == P.ERR_UNSUPPORTED, i
+
+
+def test_compact_kv_validation():
+    f = P.lib().pctree_compact_kv
+    ok = [A, 1 << 20, 1 << 16, 4, 256, 256, A, A, A, 1, 64, 16]
+    args = list(ok)
+    args[0] = None
+    assert f(*args, None) == P.ERR_INVALID_ARGUMENT
+    for i, bad in ((0, A + 8), (1, 8), (2, 24), (5, 24), (5, 8), (3, 0), (4, 0), (9, 0),
+                   (10, 0), (11, -1), (6, None), (7, A + 2), (8, None)):
+        args = list(ok)
+        args[i] = bad
+        assert f(*args, None) == P.ERR_INVALID_ARGUMENT, (i, bad)
+    for i, big in ((11, 64), (10, 1025)):
+        args = list(ok)
+        args[i] = big
+        assert f(*args, None) == P.ERR_UNSUPPORTED, i
