@@ -47,8 +47,8 @@ Readings where the paper is silent (each is also listed in the design notes):
 
 Parity pins (tests/test_oracle_pins.py): brute-force enumeration of all
 V^d paths, an exact best-first top-N search, the greedy chain of Eq. 1 for
-k = 1, the Shared-Markov control for a parent-independent head, the W = 0
-closed form, a hand-derived V = 4 example, and structural invariants.
+k = 1, the Shared-Markov control for a parent-independent head, the
+parent-independent scoring as the tree of a zero head, the W = 0 closed form, a hand-derived V = 4 example, and structural invariants.
 Parity unpinned by the paper: emission order, padding values and the
 activation rounding points above (this build's own specification).
 """
@@ -66,6 +66,7 @@ __all__ = [
     "build_tree_batch",
     "chain_decode",
     "shared_markov_rows",
+    "position_rows",
     "ancestor_mask",
     "Node",
 ]
@@ -141,6 +142,14 @@ def _layer_key(n: Node):
     return (-n.score, n.token, n.slot)
 
 
+def position_rows(L_d):
+    """Parent-independent row of one depth: log_softmax(L_d) in float64 (Eq. 2
+    with no Markov term)."""
+    z = L_d.astype(np.float64)
+    m = z.max()
+    return z - (m + np.log(np.sum(np.exp(z - m))))
+
+
 def shared_markov_rows(L, E, W, h, x_t: int, dtype: str):
     """Shared-Markov control (Sec. 5.3): the greedy chain's refined rows q_d.
 
@@ -161,13 +170,21 @@ def build_tree(L, E, W, h, x_t: int, prefix_len: int, k: int, N: int, dtype: str
     """One request's round.  ``L [B][V]``, ``E [V][r]``, ``W [r][V]``, ``h [B][r]``.
 
     ``mode="parent"`` is PCTree (every parent conditions its own row);
-    ``mode="shared"`` is the Shared-Markov control.  Returns a dict with the
-    emitted tree and the per-stage record (candidates, frontiers).
+    ``mode="shared"`` is the Shared-Markov control; ``mode="independent"`` is
+    parent-independent per-position scoring (Sec. 4: every parent of depth d
+    is expanded with the backbone's own distribution, log_softmax(L_d)).
+    Returns a dict with the emitted tree and the per-stage record
+    (candidates, frontiers).
     """
     B, V = L.shape
     kk = min(k, V)
-    shared = shared_markov_rows(L, E, W, h, x_t, dtype) if mode == "shared" else None
-    if mode not in ("parent", "shared"):
+    if mode == "shared":
+        shared = shared_markov_rows(L, E, W, h, x_t, dtype)
+    elif mode == "independent":
+        shared = [position_rows(L[d]) for d in range(B)]
+    elif mode == "parent":
+        shared = None
+    else:
         raise ValueError(mode)
 
     pool = [Node(token=int(x_t), parent=-1, depth=0, score=0.0, slot=0, path=())]
@@ -258,17 +275,22 @@ def ancestor_mask(parent: np.ndarray, count: int, N: int) -> np.ndarray:
     return words
 
 
-def chain_decode(L, E, W, h, x_t: int, dtype: str):
+def chain_decode(L, E, W, h, x_t: int, dtype: str, mode: str = "parent"):
     """The DSpark chain of Eq. 1: y_d = argmax_v z_d(y_{d-1}), y_{-1} = x_t.
 
     Ties go to the lowest token id.  Returns tokens [B+1] (x_t first) and the
-    cumulative log-probabilities [B+1] (0 for x_t).
+    cumulative log-probabilities [B+1] (0 for x_t).  A chain has one parent
+    per depth, so ``mode="shared"`` gives the same chain; ``mode="independent"``
+    takes each y_d from log_softmax(L_d) alone.
     """
     B = L.shape[0]
     toks = [int(x_t)]
     cum = [0.0]
     for d in range(B):
-        _, _, logpi = child_logprobs(L[d], E, W, h[d], toks[-1], dtype)
+        if mode == "independent":
+            logpi = position_rows(L[d])
+        else:
+            _, _, logpi = child_logprobs(L[d], E, W, h[d], toks[-1], dtype)
         y = int(np.flatnonzero(logpi == logpi.max())[0])
         toks.append(y)
         cum.append(cum[-1] + float(logpi[y]))

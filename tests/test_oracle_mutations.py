@@ -16,7 +16,7 @@ from oracle import pctree_oracle as O
 import test_oracle_pins as P
 
 PINS = [P.pin_brute_force, P.pin_best_first, P.pin_chain, P.pin_shared_markov,
-        P.pin_w_zero, P.pin_row_normalised, P.pin_hand_worked, P.pin_invariants]
+        P.pin_independent, P.pin_w_zero, P.pin_row_normalised, P.pin_hand_worked, P.pin_invariants]
 
 
 def _some_pin_fails():
@@ -83,7 +83,11 @@ def _mut_transposed_head(monkeypatch):
     monkeypatch.setattr(O, "child_logprobs", f)
 
 
-@pytest.mark.parametrize("mutate", [_mut_no_lse, _mut_silu_sign, _mut_tie_rule,
+def _mut_independent_unnormalised(monkeypatch):
+    monkeypatch.setattr(O, "position_rows", lambda L_d: L_d.astype(np.float64))  # no lse
+
+
+@pytest.mark.parametrize("mutate", [_mut_independent_unnormalised, _mut_no_lse, _mut_silu_sign, _mut_tie_rule,
                                     _mut_prune_by_token, _mut_wrong_parent,
                                     _mut_depth_desc, _mut_transposed_head])
 def test_mutation_is_caught(monkeypatch, mutate):

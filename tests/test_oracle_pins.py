@@ -104,6 +104,26 @@ def pin_shared_markov(seed=0, dtype="f32"):
                                rtol=0, atol=1e-12)
 
 
+def pin_independent(seed=0):
+    """Parent-independent scoring (Sec. 4) is the parent-conditioned tree of a
+    head that adds nothing (W = 0), and its chain takes argmax_v L_d."""
+    w = Workload("i", V=400, B=5, N=20, k=3, r=32, dtype="f32", seed=seed)
+    inp = make_inputs(w)
+    L, E, W, h, xt, pl = _single(inp)
+    a = O.build_tree(L, E, np.zeros_like(W), h, xt, pl, w.k, w.N, w.dtype, mode="parent")
+    b = O.build_tree(L, E, W, h, xt, pl, w.k, w.N, w.dtype, mode="independent")
+    for key in ("token", "parent", "depth", "position", "mask"):
+        assert np.array_equal(a[key], b[key]), key
+    np.testing.assert_allclose(a["logprob"][: a["count"]], b["logprob"][: b["count"]],
+                               rtol=0, atol=1e-12)
+    toks, cum = O.chain_decode(L, E, W, h, xt, w.dtype, mode="independent")
+    want = [xt] + [int(np.argmax(L[d])) for d in range(w.B)]
+    assert toks.tolist() == want
+    lsm = [log_softmax(L[d].astype(np.float64)) for d in range(w.B)]
+    np.testing.assert_allclose(cum[1:], np.cumsum([lsm[d][want[d + 1]] for d in range(w.B)]),
+                               rtol=0, atol=1e-12)
+
+
 def pin_w_zero(seed=0):
     w = Workload("z", V=300, B=3, N=8, k=3, r=32, dtype="f32", seed=seed)
     inp = make_inputs(w)
@@ -232,6 +252,11 @@ def test_shared_markov_differs_when_conditioned():
     b = O.build_tree(L, E, W, h, xt, pl, w.k, w.N, w.dtype, mode="shared")
     assert not (np.array_equal(a["token"], b["token"])
                 and np.allclose(a["logprob"][:a["count"]], b["logprob"][:b["count"]]))
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_independent(seed):
+    pin_independent(seed)
 
 
 def test_w_zero_closed_form():
