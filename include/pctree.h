@@ -61,7 +61,7 @@ extern "C" {
 typedef enum pctree_status {
   PCTREE_OK = 0,
   PCTREE_ERR_INVALID_ARGUMENT = 1, /* null pointer, size < 1, bad dtype, misaligned pointer */
-  PCTREE_ERR_UNSUPPORTED = 2,      /* beyond the compiled limits, or mode != 0 */
+  PCTREE_ERR_UNSUPPORTED = 2,      /* beyond the compiled limits, or an unknown mode */
   PCTREE_ERR_WORKSPACE = 3,        /* workspace null, too small or not 256-byte aligned */
   PCTREE_ERR_HIP = 4               /* a kernel launch failed */
 } pctree_status;
@@ -70,6 +70,19 @@ typedef enum pctree_dtype {
   PCTREE_F32 = 0, /* float32 base logits and head weights */
   PCTREE_BF16 = 1 /* bfloat16 base logits and head weights, fp32 accumulation */
 } pctree_dtype;
+
+/* Scoring of a parent's children (Sec. 5.3 compares the three).  Other
+ * values are PCTREE_ERR_UNSUPPORTED. */
+typedef enum pctree_mode {
+  PCTREE_MODE_PARENT = 0,      /* PCTree: every frontier parent p gets its own row
+                                  z_d(p) = L_d + Markov_d(p) (Eq. 3)              */
+  PCTREE_MODE_SHARED = 1,      /* Shared-Markov tree: the greedy chain of Eq. 1 is
+                                  built first and its row at depth d,
+                                  z_d(y_{d-1}), serves every parent of depth d     */
+  PCTREE_MODE_INDEPENDENT = 2  /* parent-independent per-position scoring (the
+                                  DDTree-style scoring named in Sec. 4): every parent
+                                  of depth d gets log_softmax(L_d)               */
+} pctree_mode;
 
 /* Problem size of one round (symbols of Sec. 4.1). */
 typedef struct pctree_shape {
@@ -80,7 +93,7 @@ typedef struct pctree_shape {
   int32_t rank;     /* r: Markov-head rank                                   */
   int32_t requests; /* R: independent requests built in one call             */
   int32_t dtype;    /* pctree_dtype of base_logits, emb and proj_t           */
-  int32_t mode;     /* 0 = parent-conditioned (PCTree); other values: UNSUPPORTED */
+  int32_t mode;     /* pctree_mode: how each parent's child row is scored      */
 } pctree_shape;
 
 /* Inputs of one round.  Request i uses base_logits[i], depth_feat[i],
@@ -144,7 +157,8 @@ pctree_status pctree_build_mask(const int32_t* parent, const int32_t* count, int
 
 /* The DSpark greedy chain of Eq. 1: y_{-1} = x_t, y_d = argmax_v z_d(y_{d-1})
  * (ties to the lowest token id).  Uses vocab, block, rank, requests, dtype and
- * mode of `shape` (topk and budget are ignored).  chain_token [R][B+1] gets
+ * mode of `shape` (topk and budget are ignored; modes PARENT and SHARED give
+ * the same chain, INDEPENDENT the chain of argmax_v L_d).  chain_token [R][B+1] gets
  * x_t, y_0..y_{B-1}; chain_logprob [R][B+1] the cumulative log-probabilities
  * (0 for x_t).  Same workspace as pctree_build_tree. */
 pctree_status pctree_chain_decode(const pctree_shape* shape, const pctree_inputs* in,

@@ -28,7 +28,7 @@ pctree_status check_shape(const pctree_shape* s) {
       s->requests < 1)
     return PCTREE_ERR_INVALID_ARGUMENT;
   if (s->dtype != PCTREE_F32 && s->dtype != PCTREE_BF16) return PCTREE_ERR_INVALID_ARGUMENT;
-  if (s->mode != 0) return PCTREE_ERR_UNSUPPORTED;
+  if (s->mode < 0 || s->mode > 2) return PCTREE_ERR_UNSUPPORTED;
   if (s->vocab > PCTREE_MAX_VOCAB || s->block > PCTREE_MAX_BLOCK || s->topk > PCTREE_MAX_TOPK ||
       s->budget > PCTREE_MAX_BUDGET || s->requests > PCTREE_MAX_REQUESTS)
     return PCTREE_ERR_UNSUPPORTED;
@@ -179,6 +179,7 @@ pctree_status pctree_build_tree(const pctree_shape* shape, const pctree_inputs* 
     if (workspace_bytes < carve_workspace(p, nullptr)) return PCTREE_ERR_WORKSPACE;
     carve_workspace(p, (char*)workspace);
     bind_inputs(p, in);
+    p.mode = shape->mode;
     p.o_token = out->token;
     p.o_parent = out->parent;
     p.o_depth = out->depth;
@@ -233,6 +234,7 @@ pctree_status pctree_chain_decode(const pctree_shape* shape, const pctree_inputs
     const ChainScratch c = chain_scratch(cs.requests, cs.block);
     char* sb = (char*)workspace + tb;
     bind_inputs(p, in);
+    p.mode = shape->mode;
     p.o_token = chain_token;
     p.o_logprob = chain_logprob;
     p.o_parent = (int*)(sb + c.parent);

@@ -159,6 +159,16 @@ __device__ __forceinline__ void put_activation(const Plan& p, size_t row, int to
   }
 }
 
+// A zero head input: the parent-independent mode scores every parent with the
+// base logits alone, z = L_d + 0 (the projection of a zero row is exactly 0).
+__device__ __forceinline__ void put_zero_activation(const Plan& p, size_t row, int j) {
+  const size_t o = row * p.r + j;
+  if (p.dtype)
+    ((uint16_t*)p.U)[o] = 0;
+  else
+    ((float*)p.U)[o] = 0.0f;
+}
+
 // Selection state of a round: the frontier (slot-indexed, kk per request) and
 // the running global top-N (sorted keys and pool ids, N per request).  It
 // lives in the workspace for the multi-launch form and in the selector
@@ -483,8 +493,12 @@ __global__ __launch_bounds__(kEmitThreads) void prologue_kernel(Plan p) {
     p.front_tok[req * p.kk] = root;
     p.front_score[req * p.kk] = 0.0f;
   }
-  for (int j = tid; j < p.r; j += blockDim.x)
-    put_activation(p, (size_t)req * p.kk, root, j, p.h[(size_t)req * p.B * p.r + j]);
+  for (int j = tid; j < p.r; j += blockDim.x) {
+    if (p.mode == 2)
+      put_zero_activation(p, (size_t)req * p.kk, j);
+    else
+      put_activation(p, (size_t)req * p.kk, root, j, p.h[(size_t)req * p.B * p.r + j]);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1284,7 +1298,7 @@ struct SelShared {
 // into the running global top-N (Sec. 4.2) and write the next head input.
 // Needs blockDim >= 512 and nreq * P * k' <= 256.
 __device__ void stage_select(const Plan& p, const State& st, int d, int P, int req0, int nreq,
-                             SelShared& sh, bool act, bool bcast) {
+                             SelShared& sh, bool act, bool bcast, bool shared = false) {
   const int tid = threadIdx.x;
   const int kk = p.kk;
   const int per_req = P * kk;
@@ -1300,7 +1314,7 @@ __device__ void stage_select(const Plan& p, const State& st, int d, int P, int r
     const int pr = ci / kk;
     const int j = ci - pr * kk;
     const int req = req0 + rq;
-    const int lrow = rq * P + pr;
+    const int lrow = shared ? rq : rq * P + pr;  // shared: one row serves every parent
     const uint64_t ck = sh.rowkeys[lrow][j];
     // every row holds >= k' real keys (V >= k'); the clamp only keeps a
     // corrupted key from indexing out of bounds
@@ -1842,7 +1856,24 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, i
     }
   }
   __syncthreads();
-  stage_select(p, global_state(p), d, P, req, 1, ssh, true, false);
+  if (p.mode == 0) {
+    stage_select(p, global_state(p), d, P, req, 1, ssh, true, false);
+    return;
+  }
+  // Shared-Markov and parent-independent modes: the one row of the stage
+  // (P = 1) serves every frontier parent of the tree
+  stage_select(p, global_state(p), d, d == 0 ? 1 : p.kk, req, 1, ssh, false, false, true);
+  if (d + 1 < p.B) {
+    // next head input: the greedy chain's token (Shared-Markov), or zero
+    const int tok = min(max(child_key_token(ssh.rowkeys[0][0]), 0), p.V - 1);
+    const float* hrow = p.h + ((size_t)req * p.B + d + 1) * p.r;
+    for (int j = threadIdx.x; j < p.r; j += blockDim.x) {
+      if (p.mode == 2)
+        put_zero_activation(p, (size_t)req * p.kk, j);
+      else
+        put_activation(p, (size_t)req * p.kk, tok, j, hrow[j]);
+    }
+  }
 }
 
 // Zero the words the persistent round polls (slice partials of every stage,
@@ -1987,7 +2018,7 @@ DeviceInfo device_info() {
 }  // namespace
 
 hipError_t launch_round(const Plan& p0, hipStream_t st) {
-  const bool narrow = p0.R * p0.kk <= kNarrowRows;
+  const bool narrow = p0.R * p0.kk <= kNarrowRows && p0.mode == 0;
   Plan p = p0;
   DeviceInfo di;
   RoundFn rfn = nullptr;
@@ -2059,7 +2090,8 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
   const StageFn head = head_fn(p);
   const StageFn sel = select_fn(p.kmax);
   for (int d = 0; d < p.B; ++d) {
-    const int P = d == 0 ? 1 : p.kk;
+    // head rows per request: the frontier, or the one shared row of the stage
+    const int P = (d == 0 || p.mode != 0) ? 1 : p.kk;
     const int cb = (p.R * P + kTile - 1) / kTile;
     const bool prof = profile_on();
     if (prof) profile_mark(st, "head_kernel");

@@ -80,7 +80,7 @@ struct Plan {
   int* req_bad;      // [R] root token outside [0, V)
   uint64_t* front_w; // [stages][rows_max] frontier of each stage (persistent form)
   uint32_t tag;      // this call's tag, 1 .. kTagMask (published words carry it)
-  int pad_;
+  int mode;          // 0 parent-conditioned, 1 Shared-Markov, 2 parent-independent
   long long spin_ticks;  // device wall-clock ticks a wait may last before aborting
   int lds_tiles;         // W tiles a streaming block keeps in LDS for the whole round
   int lds_top_offset;    // byte offset of the keeper's running top-N in the dynamic LDS

@@ -26,6 +26,9 @@ __all__ = [
     "status_string",
     "F32",
     "BF16",
+    "MODE_PARENT",
+    "MODE_SHARED",
+    "MODE_INDEPENDENT",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -33,6 +36,7 @@ LIB_PATH = os.path.join(_HERE, "libpctree.so")
 
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 F32, BF16 = 0, 1
+MODE_PARENT, MODE_SHARED, MODE_INDEPENDENT = 0, 1, 2  # pctree_mode
 
 
 class PCTreeError(RuntimeError):
@@ -158,8 +162,9 @@ class TreeBuilder:
     stream and returns the output tensors (overwritten by the next call).
     """
 
-    def __init__(self, V, B, N, k, r, R=1, dtype=BF16, device="cuda", mask=True, trace=False):
-        self.shape = make_shape(V, B, N, k, r, R, dtype)
+    def __init__(self, V, B, N, k, r, R=1, dtype=BF16, device="cuda", mask=True, trace=False,
+                 mode=MODE_PARENT):
+        self.shape = make_shape(V, B, N, k, r, R, dtype, mode)
         nbytes = int(lib().pctree_workspace_bytes(ctypes.byref(self.shape)))
         if nbytes == 0:
             _check(lib().pctree_build_tree(ctypes.byref(self.shape), None, None, None, None, 0,
@@ -206,14 +211,16 @@ class TreeBuilder:
         return self.out
 
 
-def build_tree(L, E, Wt, h, root, prefix_len, k, N, *, mask=True, trace=False, stream=None):
+def build_tree(L, E, Wt, h, root, prefix_len, k, N, *, mask=True, trace=False, stream=None,
+               mode=MODE_PARENT):
     """One round for tensors ``L [R][B][V]``, ``E [V][r]``, ``Wt [V][r]``, ``h [R][B][r]``.
 
     Returns a dict of freshly allocated output tensors (see include/pctree.h).
     """
     R, B, V = L.shape
     r = E.shape[1]
-    b = TreeBuilder(V, B, N, k, r, R, _dtype_code(L), device=L.device, mask=mask, trace=trace)
+    b = TreeBuilder(V, B, N, k, r, R, _dtype_code(L), device=L.device, mask=mask, trace=trace,
+                    mode=mode)
     return b.run(L, E, Wt, h, root, prefix_len, stream=stream)
 
 
@@ -243,13 +250,13 @@ def build_mask(parent, count, stream=None):
     return mask
 
 
-def chain_decode(L, E, Wt, h, root, prefix_len=None, stream=None):
+def chain_decode(L, E, Wt, h, root, prefix_len=None, stream=None, mode=MODE_PARENT):
     """The greedy chain of Eq. 1: returns (tokens [R][B+1], cumulative logprobs [R][B+1])."""
     R, B, V = L.shape
     r = E.shape[1]
     if prefix_len is None:
         prefix_len = torch.zeros(R, dtype=torch.int32, device=L.device)
-    shape = make_shape(V, B, 1, 1, r, R, _dtype_code(L))
+    shape = make_shape(V, B, 1, 1, r, R, _dtype_code(L), mode)
     nbytes = int(lib().pctree_workspace_bytes(ctypes.byref(shape)))
     ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=L.device)
     toks = torch.empty(R, B + 1, dtype=torch.int32, device=L.device)

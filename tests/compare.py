@@ -42,6 +42,22 @@ class Rows:
         return self.cache[key]
 
 
+class ModeRows:
+    """Oracle rows of the two control modes: one row per depth serves every
+    parent (the Shared-Markov chain's rows, or log_softmax(L_d))."""
+
+    def __init__(self, L, E, W64, h, x_t, dtype, mode):
+        if mode == "shared":
+            self.rows = O.shared_markov_rows(L, E, W64, h, int(x_t), dtype)
+        elif mode == "independent":
+            self.rows = [O.position_rows(L[d]) for d in range(L.shape[0])]
+        else:
+            raise ValueError(mode)
+
+    def __call__(self, d, tok):
+        return self.rows[d]
+
+
 def _np(x):
     return x.detach().cpu().numpy() if hasattr(x, "detach") else np.asarray(x)
 
@@ -178,14 +194,19 @@ def gpu_to_numpy(out, req):
     return g
 
 
-def compare_batch(out, inp, k, N, requests=None):
+def compare_batch(out, inp, k, N, requests=None, mode="parent"):
     """Compare every request (or the listed ones) of a GPU batch output."""
     w = inp["workload"]
     W64 = inp["W"].astype(np.float64)
     reports = []
     for req in (range(inp["L"].shape[0]) if requests is None else requests):
         g = gpu_to_numpy(out, req)
-        reports.append(compare_request(g, inp["L"][req], inp["E"], W64, inp["h"][req],
-                                       int(inp["root"][req]), int(inp["prefix_len"][req]), k, N,
-                                       w.dtype))
+        L, h, x_t, pl = inp["L"][req], inp["h"][req], int(inp["root"][req]), \
+            int(inp["prefix_len"][req])
+        rows = oracle = None
+        if mode != "parent":
+            rows = ModeRows(L, inp["E"], W64, h, x_t, w.dtype, mode)
+            oracle = O.build_tree(L, inp["E"], W64, h, x_t, pl, k, N, w.dtype, mode=mode)
+        reports.append(compare_request(g, L, inp["E"], W64, h, x_t, pl, k, N, w.dtype,
+                                       rows=rows, oracle=oracle))
     return reports

@@ -77,7 +77,8 @@ def test_nonpositive_sizes_are_invalid(field):
 
 @pytest.mark.parametrize("kw,code", [
     (dict(dtype=7), P.ERR_INVALID_ARGUMENT),
-    (dict(mode=1), P.ERR_UNSUPPORTED),
+    (dict(mode=3), P.ERR_UNSUPPORTED),
+    (dict(mode=-1), P.ERR_UNSUPPORTED),
     (dict(vocab=(1 << 20) + 1), P.ERR_UNSUPPORTED),
     (dict(block=64), P.ERR_UNSUPPORTED),
     (dict(topk=17), P.ERR_UNSUPPORTED),
@@ -144,7 +145,7 @@ def test_chain_decode_validation():
     f = P.lib().pctree_chain_decode
     s = shape(topk=0, budget=0)  # ignored by the chain
     vp = ctypes.c_void_p
-    assert f(ctypes.byref(shape(mode=2)), ctypes.byref(inputs()), vp(A), vp(A), vp(A * 16),
+    assert f(ctypes.byref(shape(mode=3)), ctypes.byref(inputs()), vp(A), vp(A), vp(A * 16),
              1 << 30, None) == P.ERR_UNSUPPORTED
     assert f(ctypes.byref(s), ctypes.byref(inputs()), None, vp(A), vp(A * 16), 1 << 30,
              None) == P.ERR_INVALID_ARGUMENT
