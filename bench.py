@@ -87,6 +87,94 @@ def cpu_baseline(inp, w, seconds):
                       f"in {el:.1f} s; BLAS threads {threads}, os.cpu_count() {os.cpu_count()}"}
 
 
+def _event_us(fn, reps):
+    import torch
+
+    fn()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        fn()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) * 1000.0 / reps
+
+
+def time_verify(P, builder, w, inp, reps=200):
+    """The verification steps after one round of the workload: retrieve rows,
+    greedy acceptance against synthetic target predictions, and compaction of
+    a Qwen3-4B-shaped KV cache (36 layers x K/V, 8 KV heads x 128 dims, bf16)."""
+    import numpy as np
+    import torch
+    from paper_2608_02123_amd.synth import target_next
+
+    log("[bench] verification steps")
+    out = builder.launch()
+    torch.cuda.synchronize()
+    tok = out["token"].cpu().numpy()
+    par = out["parent"].cpu().numpy()
+    cnt = out["count"].cpu().numpy()
+    rng = np.random.default_rng(1)
+    tn = np.stack([target_next(rng, tok[i], par[i], int(cnt[i]), w.V, 0.8)
+                   for i in range(w.R)])
+    tn = torch.from_numpy(tn).cuda()
+    groups, slot = 72, 8 * 128
+    prefix = inp["prefix_len"]
+    cap = int(prefix.max()) + w.N
+    cache = torch.zeros(w.R, groups, cap, slot, dtype=torch.bfloat16, device="cuda")
+    pre = torch.from_numpy(prefix).cuda()
+    rows, nrows = P.build_retrieve(out["parent"], out["count"], w.B)
+    acc = P.accept_greedy(out["token"], rows, nrows, tn)
+    torch.cuda.synchronize()
+    a_len = acc["accept_len"].cpu().numpy()
+    nodes = acc["accept_node"].cpu().numpy()
+    moved = sum(int(sum(1 for m in range(a_len[i] + 1) if nodes[i, m] != m)) for i in range(w.R))
+    # the C entry points with their arguments marshalled once, so that the
+    # events see the kernels rather than the Python wrappers
+    import ctypes
+    L = P.lib()
+    vp = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    ra = (vp(out["parent"]), vp(out["count"]), w.R, w.N, w.B, vp(rows), vp(nrows), st)
+    aa = (vp(out["token"]), vp(rows), vp(nrows), vp(tn), w.R, w.N, w.B, vp(acc["accept_len"]),
+          vp(acc["accept_row"]), vp(acc["accept_node"]), vp(acc["bonus"]), st)
+    es = cache.element_size()
+    ca = (vp(cache), cache.stride(0) * es, cache.stride(1) * es, groups, cap, slot * es, vp(pre),
+          vp(acc["accept_node"]), vp(acc["accept_len"]), w.R, w.N, w.B, st)
+    us_r = _event_us(lambda: L.pctree_build_retrieve(*ra), reps)
+    us_a = _event_us(lambda: L.pctree_accept_greedy(*aa), reps)
+    us_c = _event_us(lambda: L.pctree_compact_kv(*ca), reps)
+    return {"retrieve_us": us_r, "accept_us": us_a, "compact_us": us_c,
+            "accept_len": [int(x) for x in a_len], "nrows": [int(x) for x in nrows.cpu()],
+            "compact_bytes": 2 * moved * groups * slot * 2,
+            "kv": "72 groups (36 layers x K/V) x 8 heads x 128 dims bf16 per slot",
+            "target": "synthetic: a child's token with p = 0.8 at each node, else uniform"}
+
+
+def time_sweeps(P, w, inp, dev, reps=30):
+    """us/round of the two control scorings (Sec. 5.3) and of k and N sweeps
+    (the paper's ablations over the branching factor and the budget)."""
+    import torch
+
+    log("[bench] sweeps")
+    dt = P.BF16 if w.dtype == "bf16" else P.F32
+
+    def us(k, N, mode=P.MODE_PARENT):
+        b = P.TreeBuilder(w.V, w.B, N, k, w.r, w.R, dt, mask=True, mode=mode)
+        b.bind(**dev)
+        for _ in range(3):
+            b.launch()
+        return _event_us(b.launch, reps)
+
+    return {
+        "modes_us": {"parent": us(w.k, w.N), "shared": us(w.k, w.N, P.MODE_SHARED),
+                     "independent": us(w.k, w.N, P.MODE_INDEPENDENT)},
+        "k_us": {str(k): us(k, w.N) for k in (1, 2, 4, 8, 16)},
+        "N_us": {str(N): us(w.k, N) for N in (8, 16, 32, 64, 128, 256)},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -96,6 +184,10 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cold-steps", type=int, default=50)
+    ap.add_argument("--no-verify", action="store_true",
+                    help="skip timing the verification steps after the round")
+    ap.add_argument("--sweep", action="store_true",
+                    help="also time the two control scorings and k / N sweeps")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run three 256 MiB device-to-device passes (an elementwise "
                          "negation: 256 MiB read, 256 MiB written), the reference for HBM counters")
@@ -175,6 +267,9 @@ def main():
     cold_ms = sorted(x.elapsed_time(y) for x, y in cold)
     cold_med = cold_ms[len(cold_ms) // 2] if cold_ms else None
 
+    verify = None if args.no_verify else time_verify(P, builder, w, inp)
+    sweep = time_sweeps(P, w, inp, dev) if args.sweep else None
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"[bench] cpu baseline (~{args.cpu_seconds:.0f} s)")
@@ -210,6 +305,10 @@ def main():
         "cpu_baseline": cpu,
         "wall_s_timed_region": wall,
     }
+    if verify is not None:
+        line["verify"] = verify
+    if sweep is not None:
+        line["sweep"] = sweep
     print(json.dumps(line), flush=True)
 
 
