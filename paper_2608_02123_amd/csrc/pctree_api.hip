@@ -107,7 +107,9 @@ void plan_shape(Plan& p, int V, int B, int N, int k, int r, int R, int dtype) {
   p.kmax = pow2ceil(p.kk);
   p.nchunk = dtype ? r / 32 : r / 16;
   p.ntiles = (V + kTile - 1) / kTile;
-  p.tiles_per_slice = std::max(4, (p.ntiles + kSlicesMax - 1) / kSlicesMax);
+  // multi-launch form: about one slice per CU of a 256-CU device (the
+  // persistent form sizes its slices from the device at launch)
+  p.tiles_per_slice = std::max(4, (p.ntiles + 255) / 256);
   p.G = (p.ntiles + p.tiles_per_slice - 1) / p.tiles_per_slice;
   p.maxpool = 1 + p.kk + (B - 1) * p.kk * p.kk;
   p.rows_max = R * p.kk;
@@ -139,6 +141,8 @@ size_t carve_workspace(Plan& p, char* base) {
   p.part_hd = (uint64_t*)take(parts * kRecWords * sizeof(uint64_t));
   p.req_bad = (int*)take(R * sizeof(int));
   p.front_w = (uint64_t*)take((size_t)p.stages * p.rows_max * sizeof(uint64_t));
+  p.mrow_key = (uint64_t*)take((size_t)p.rows_max * p.kmax * sizeof(uint64_t));
+  p.mrow_lse = (float*)take((size_t)p.rows_max * sizeof(float));
   return off;
 }
 

@@ -1793,7 +1793,200 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
 template <int DT, int NCMAX, int KMAX>
 __global__ __launch_bounds__(kHeadThreads) void head_kernel(Plan p, int d, int P) {
   __shared__ HeadShared<KMAX, kHeadThreads / 64> hsh;
-  head_slice<DT, NCMAX, KMAX, kHeadThreads / 64>(p, d, P, blockIdx.y, blockIdx.x, hsh);
+  // Workgroups go to the 8 XCDs in turn (id i to XCD i % 8).  The column
+  // blocks of one V-slice get consecutive ids within one XCD, so they run
+  // side by side there and all but the first read the slice's W from that
+  // XCD's L2.  The grid has 8 * ceil(G / 8) * ncb workgroups.
+  const int ncb = (p.R * P + kTile - 1) / kTile;
+  const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int cb = j % ncb;
+  const int slice = (j / ncb) * 8 + x;
+  if (slice >= p.G) return;
+  head_slice<DT, NCMAX, KMAX, kHeadThreads / 64>(p, d, P, cb, slice, hsh);
+}
+
+// After the rows of stage d are in sh (top-k' children, lse): the stage
+// selection of request req, and for the two control modes the next stage's
+// single head input.
+__device__ void select_tail(const Plan& p, int d, int P, int req, SelShared& ssh) {
+  if (p.mode == 0) {
+    stage_select(p, global_state(p), d, P, req, 1, ssh, true, false);
+    return;
+  }
+  // Shared-Markov and parent-independent modes: the one row of the stage
+  // (P = 1) serves every frontier parent of the tree
+  stage_select(p, global_state(p), d, d == 0 ? 1 : p.kk, req, 1, ssh, false, false, true);
+  if (d + 1 < p.B) {
+    // next head input: the greedy chain's token (Shared-Markov), or zero
+    const int tok = min(max(child_key_token(ssh.rowkeys[0][0]), 0), p.V - 1);
+    const float* hrow = p.h + ((size_t)req * p.B + d + 1) * p.r;
+    for (int j = threadIdx.x; j < p.r; j += blockDim.x) {
+      if (p.mode == 2)
+        put_zero_activation(p, (size_t)req * p.kk, j);
+      else
+        put_activation(p, (size_t)req * p.kk, tok, j, hrow[j]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// multi-launch form, wide frontiers (more than 16 rows per stage)
+// ---------------------------------------------------------------------------
+constexpr int kWideWaves = 8;      // column blocks of 16 rows one workgroup serves
+constexpr int kMergeThreads = 256;
+
+// Publish one wave's rows (column block) of a slice: the four lanes of a row
+// merge their lists and (max, sum) pairs, and the first writes the slice
+// record and list of stage 0's buffers (read by the next launch).
+template <int KMAX>
+__device__ __forceinline__ void publish_wave(const Plan& p, const HeadLane& h, int slice,
+                                             RowAcc<KMAX>& r) {
+  float m = r.m, sum = r.s;
+  list_merge_pair<16>(r.list);
+  lse_combine_pair<16>(m, sum);
+  list_merge_pair<32>(r.list);
+  lse_combine_pair<32>(m, sum);
+  if (h.grp == 0 && h.row_ok) {
+    uint64_t* hd = slice_record(p, 0, h.row) + slice;
+#pragma unroll
+    for (int i = 0; i < kHeadKeys; ++i)
+      __hip_atomic_store(hd + i * kSlicesMax, (i < KMAX ? r.list[i < KMAX ? i : 0] : 0ull) | p.tag,
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(hd + kHeadKeys * kSlicesMax, ((uint64_t)p.tag << 32) | __float_as_uint(sum),
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint64_t* dst = p.part_key + ((size_t)h.row * kSlicesMax + slice) * KMAX;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i)
+      __hip_atomic_store(dst + i, r.list[i] | p.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// One V-slice for up to kWideWaves column blocks of 16 frontier rows (wave w
+// holds block 8 * group + w, its rows' head input in registers for the whole
+// slice).  Each W tile is read from memory once per workgroup: all waves
+// fetch a share of its rank chunks and store them in LDS in MFMA fragment
+// order, then every wave multiplies the whole tile with its own rows.  Two
+// LDS buffers: tile t + 1 is fetched while tile t is multiplied.  The grid
+// has 8 * ceil(G / 8) * (column groups) workgroups, in the XCD-aware order
+// of head_kernel.
+template <int DT, int NCMAX, int KMAX>
+__global__ __launch_bounds__(kWideWaves * 64) void head_wide_kernel(Plan p, int d, int P) {
+  constexpr int KC = DT ? 32 : 16;  // rank elements per 16x16 MFMA step
+  constexpr int ESZ = DT ? 2 : 4;
+  constexpr int CPW = (NCMAX + kWideWaves - 1) / kWideWaves;  // chunks one wave fetches
+  __shared__ u32x4 tiles[2][NCMAX][64];
+  const int ncb = (p.R * P + kTile - 1) / kTile;
+  const int ngrp = (ncb + kWideWaves - 1) / kWideWaves;
+  const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int grp = j % ngrp;
+  const int slice = (j / ngrp) * 8 + x;
+  if (slice >= p.G) return;  // the whole workgroup
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int cb = grp * kWideWaves + wave;
+  const bool live = cb < ncb;  // waves past the last block only fetch
+  const HeadLane h(p, P, live ? cb : 0);
+  u32x4 bfrag[NCMAX];
+  if (live) load_bfrag<DT, NCMAX>(p, h, bfrag);
+  RowAcc<KMAX> r;
+  r.init();
+  const int t0 = slice * p.tiles_per_slice;
+  const int t1 = min(t0 + p.tiles_per_slice, p.ntiles);
+  // lane l fetches what lane l of a consumer feeds the MFMA: token l % 16 of
+  // the tile (clamped into the vocabulary), rank group l / 16; chunks past
+  // the rank re-read the last one (finite values that meet zero B fragments)
+  u32x4 stage[CPW];
+  auto fetch = [&](int t) {
+    const int tok = min(t * kTile + (lane & 15), p.V - 1);
+    const char* wrow = (const char*)p.Wt + ((size_t)tok * p.r + (lane >> 4) * (KC / 4)) * ESZ;
+#pragma unroll
+    for (int q = 0; q < CPW; ++q) {
+      const int c = wave + q * kWideWaves;
+      if (c < NCMAX) stage[q] = *(const u32x4*)(wrow + (size_t)min(c, p.nchunk - 1) * KC * ESZ);
+    }
+  };
+  auto put = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < CPW; ++q) {
+      const int c = wave + q * kWideWaves;
+      if (c < NCMAX) tiles[buf][c][lane] = stage[q];
+    }
+  };
+  uint32_t l[4] = {0u, 0u, 0u, 0u}, ln[4] = {0u, 0u, 0u, 0u};
+  fetch(t0);
+  if (live) load_lfrag<DT>(p, h, d, t0, l);
+  put(0);
+  __syncthreads();
+  for (int t = t0; t < t1; ++t) {
+    const int buf = (t - t0) & 1;
+    const bool more = t + 1 < t1;
+    if (more) {
+      fetch(t + 1);
+      if (live) load_lfrag<DT>(p, h, d, t + 1, ln);
+    }
+    if (live) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < NCMAX; ++c) acc = mfma_chunk<DT>(tiles[buf][c][lane], bfrag[c], acc);
+      tile_epilogue<DT, KMAX>(p, h, acc, l, t, h.row_ok, r);
+    }
+    if (more) put(buf ^ 1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) l[i] = ln[i];
+    __syncthreads();
+  }
+  if (live) publish_wave<KMAX>(p, h, slice, r);
+}
+
+// One workgroup per frontier row of the stage: merge the row's G slice lists
+// and (max, sum) records into its top-KMAX children and lse (lanes over
+// slices, then xor trees over the wave and the workgroup).
+template <int KMAX>
+__global__ __launch_bounds__(kMergeThreads) void rowmerge_kernel(Plan p) {
+  constexpr int NW = kMergeThreads / 64;
+  __shared__ uint64_t sh_list[NW][KMAX];
+  __shared__ float2 sh_ms[NW];
+  const int grow = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint64_t list[KMAX];
+#pragma unroll
+  for (int i = 0; i < KMAX; ++i) list[i] = 0;
+  float m = kNegBig, s = 0.0f;
+  const uint64_t* rec = slice_record(p, 0, grow);
+  for (int g = threadIdx.x; g < p.G; g += kMergeThreads) {
+    uint64_t other[KMAX];
+    const uint64_t* src = p.part_key + ((size_t)grow * kSlicesMax + g) * KMAX;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) other[i] = src[i];
+    list_merge(list, other);
+    lse_combine(m, s, child_key_value(rec[g]), __uint_as_float((uint32_t)rec[kHeadKeys * kSlicesMax + g]));
+  }
+#pragma unroll
+  for (int mask = 1; mask < 64; mask <<= 1) {
+    list_merge_xor(list, mask);
+    lse_combine_xor(m, s, mask);
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) sh_list[wave][i] = list[i];
+    sh_ms[wave] = make_float2(m, s);
+  }
+  __syncthreads();
+  if (wave == 0) {
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) list[i] = lane < NW ? sh_list[lane][i] : 0;
+    m = lane < NW ? sh_ms[lane].x : kNegBig;
+    s = lane < NW ? sh_ms[lane].y : 0.0f;
+#pragma unroll
+    for (int mask = 1; mask < NW; mask <<= 1) {
+      list_merge_xor(list, mask);
+      lse_combine_xor(m, s, mask);
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) p.mrow_key[(size_t)grow * KMAX + i] = list[i];
+      p.mrow_lse[grow] = m + logf(s);
+    }
+  }
 }
 
 // One WG per request: merge the G slice lists of its P rows (waves per row,
@@ -1856,24 +2049,23 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, i
     }
   }
   __syncthreads();
-  if (p.mode == 0) {
-    stage_select(p, global_state(p), d, P, req, 1, ssh, true, false);
-    return;
+  select_tail(p, d, P, req, ssh);
+}
+
+// Rows of a stage merged by rowmerge_kernel: one WG per request reads its P
+// rows' top-k' children and lse, then the shared stage selection.
+template <int KMAX>
+__global__ __launch_bounds__(kSelectThreads) void select_merged_kernel(Plan p, int d, int P) {
+  __shared__ SelShared ssh;
+  const int req = blockIdx.x;
+  for (int e = threadIdx.x; e < P * KMAX; e += blockDim.x) {
+    const int prow = e / KMAX, i = e - prow * KMAX;
+    ssh.rowkeys[prow][i] = p.mrow_key[(size_t)(req * P + prow) * KMAX + i];
   }
-  // Shared-Markov and parent-independent modes: the one row of the stage
-  // (P = 1) serves every frontier parent of the tree
-  stage_select(p, global_state(p), d, d == 0 ? 1 : p.kk, req, 1, ssh, false, false, true);
-  if (d + 1 < p.B) {
-    // next head input: the greedy chain's token (Shared-Markov), or zero
-    const int tok = min(max(child_key_token(ssh.rowkeys[0][0]), 0), p.V - 1);
-    const float* hrow = p.h + ((size_t)req * p.B + d + 1) * p.r;
-    for (int j = threadIdx.x; j < p.r; j += blockDim.x) {
-      if (p.mode == 2)
-        put_zero_activation(p, (size_t)req * p.kk, j);
-      else
-        put_activation(p, (size_t)req * p.kk, tok, j, hrow[j]);
-    }
-  }
+  for (int prow = threadIdx.x; prow < P; prow += blockDim.x)
+    ssh.lse[prow] = p.mrow_lse[req * P + prow];
+  __syncthreads();
+  select_tail(p, d, P, req, ssh);
 }
 
 // Zero the words the persistent round polls (slice partials of every stage,
@@ -1956,6 +2148,7 @@ typedef void (*RoundFn)(Plan);
   PCTREE_KMAX_SWITCH(KERNEL, 0, 8, (p).kmax)
 
 StageFn head_fn(const Plan& p) { PCTREE_DISPATCH(head_kernel, p) }
+StageFn head_wide_fn(const Plan& p) { PCTREE_DISPATCH(head_wide_kernel, p) }
 
 // NCMAX of the instantiation PCTREE_DISPATCH picks.
 int nchunk_max(const Plan& p) {
@@ -1975,6 +2168,27 @@ RoundFn round_fn(const Plan& p) {
   }
   if (p.nchunk <= 2) { PCTREE_ROUND_KMAX_SWITCH(round_kernel, 0, 2, p.kmax, fold) }
   PCTREE_ROUND_KMAX_SWITCH(round_kernel, 0, 8, p.kmax, fold)
+}
+
+typedef void (*MergeFn)(Plan);
+MergeFn rowmerge_fn(int kmax) {
+  switch (kmax) {
+    case 1: return rowmerge_kernel<1>;
+    case 2: return rowmerge_kernel<2>;
+    case 4: return rowmerge_kernel<4>;
+    case 8: return rowmerge_kernel<8>;
+    default: return rowmerge_kernel<16>;
+  }
+}
+
+StageFn select_merged_fn(int kmax) {
+  switch (kmax) {
+    case 1: return select_merged_kernel<1>;
+    case 2: return select_merged_kernel<2>;
+    case 4: return select_merged_kernel<4>;
+    case 8: return select_merged_kernel<8>;
+    default: return select_merged_kernel<16>;
+  }
 }
 
 StageFn select_fn(int kmax) {
@@ -2089,15 +2303,31 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
   hipLaunchKernelGGL(prologue_kernel, dim3(p.R), dim3(kEmitThreads), 0, st, p);
   const StageFn head = head_fn(p);
   const StageFn sel = select_fn(p.kmax);
+  const StageFn head_wide = head_wide_fn(p);
+  const MergeFn merge = rowmerge_fn(p.kmax);
+  const StageFn sel_merged = select_merged_fn(p.kmax);
+  const int slices8 = (p.G + 7) / 8 * 8;
   for (int d = 0; d < p.B; ++d) {
     // head rows per request: the frontier, or the one shared row of the stage
     const int P = (d == 0 || p.mode != 0) ? 1 : p.kk;
     const int cb = (p.R * P + kTile - 1) / kTile;
     const bool prof = profile_on();
-    if (prof) profile_mark(st, "head_kernel");
-    hipLaunchKernelGGL(head, dim3(p.G, cb), dim3(kHeadThreads), 0, st, p, d, P);
-    if (prof) profile_mark(st, "head_kernel");
-    hipLaunchKernelGGL(sel, dim3(p.R), dim3(kSelectThreads), 0, st, p, d, P);
+    if (cb == 1) {
+      // one column block: 4 waves split the slice's tiles; one WG per
+      // request merges and selects
+      if (prof) profile_mark(st, "head_kernel");
+      hipLaunchKernelGGL(head, dim3(slices8 * cb), dim3(kHeadThreads), 0, st, p, d, P);
+      if (prof) profile_mark(st, "head_kernel");
+      hipLaunchKernelGGL(sel, dim3(p.R), dim3(kSelectThreads), 0, st, p, d, P);
+    } else {
+      // wide: 8 column blocks share each W tile; rows merge in parallel
+      const int ngrp = (cb + kWideWaves - 1) / kWideWaves;
+      if (prof) profile_mark(st, "head_wide_kernel");
+      hipLaunchKernelGGL(head_wide, dim3(slices8 * ngrp), dim3(kWideWaves * 64), 0, st, p, d, P);
+      if (prof) profile_mark(st, "head_wide_kernel");
+      hipLaunchKernelGGL(merge, dim3(p.R * P), dim3(kMergeThreads), 0, st, p);
+      hipLaunchKernelGGL(sel_merged, dim3(p.R), dim3(kSelectThreads), 0, st, p, d, P);
+    }
   }
   hipLaunchKernelGGL(emit_kernel, dim3(p.R), dim3(kEmitThreads), 0, st, p);
   return hipGetLastError();

@@ -79,6 +79,8 @@ struct Plan {
   uint64_t* part_hd; // [stages][rows_max][kRecWords][kSlicesMax] slice records
   int* req_bad;      // [R] root token outside [0, V)
   uint64_t* front_w; // [stages][rows_max] frontier of each stage (persistent form)
+  uint64_t* mrow_key;// [rows_max][kmax] merged top-k' children of each row (wide stages)
+  float* mrow_lse;   // [rows_max] merged lse of each row (wide stages)
   uint32_t tag;      // this call's tag, 1 .. kTagMask (published words carry it)
   int mode;          // 0 parent-conditioned, 1 Shared-Markov, 2 parent-independent
   long long spin_ticks;  // device wall-clock ticks a wait may last before aborting

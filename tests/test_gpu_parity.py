@@ -82,6 +82,13 @@ SHAPES = [
     (20000, 5, 256, 16, 128, 1, "bf16"),
     (3000, 6, 33, 1, 96, 4, "bf16"),   # k = 1: the chain
     (2500, 4, 50, 5, 128, 1, "f32"),   # widest f32 rank
+    # more than 16 frontier rows per stage: the wide multi-launch stages
+    (2000, 3, 48, 16, 64, 2, "bf16"),  # two column blocks of one group
+    (3000, 4, 40, 8, 128, 5, "f32"),   # three blocks, f32 rank 128
+    (700, 3, 30, 5, 32, 9, "bf16"),    # k' = 5 in lists of 8, 45 rows
+    (33, 3, 20, 6, 32, 20, "bf16"),    # 20 requests: wide from stage 0; ragged last tile
+    (500, 2, 16, 16, 32, 256, "bf16"),  # the request limit: 4096 rows, 32 column groups
+    (9000, 3, 64, 16, 512, 3, "bf16"),  # the largest rank
 ]
 
 
