@@ -32,7 +32,8 @@ from dataclasses import dataclass, field
 import numpy as np
 
 __all__ = ["Workload", "CONFIGS", "make_inputs", "round_to_bf16", "bf16_bits",
-           "random_tree", "target_next", "make_kv_cache"]
+           "random_tree", "target_next", "make_kv_cache", "ATTN_SHAPES",
+           "make_attention_inputs"]
 
 
 @dataclass(frozen=True)
@@ -223,3 +224,38 @@ def make_kv_cache(rng: np.random.Generator, groups: int, capacity: int, width: i
     bits = rng.integers(0, 1 << 16, size=(groups, capacity, width), dtype=np.uint32)
     bits &= ~np.uint32(0x4000)  # exponent below all ones: finite values
     return bits.astype(np.uint16)
+
+
+# ---------------------------------------------------------------------------
+# Inputs of one tree-masked verification attention layer
+# ---------------------------------------------------------------------------
+
+# (query heads, key/value heads, head dimension) of the Qwen3 targets'
+# attention layers (grouped-query attention).
+ATTN_SHAPES = {
+    "qwen3_4b": (32, 8, 128),
+    "qwen3_8b": (32, 8, 128),
+    "qwen3_14b": (40, 8, 128),
+}
+
+
+def make_attention_inputs(rng: np.random.Generator, R: int, N: int, Hq: int, Hkv: int, D: int,
+                          prefix_len: np.ndarray, count: np.ndarray, capacity: int,
+                          q_scale: float = 1.0) -> dict:
+    """Synthetic operands of one attention layer of the verification forward.
+
+    ``q [R][N][Hq][D]`` (``N(0, q_scale^2)``), ``k`` and ``v [R][Hkv][capacity][D]``
+    (``N(0, 1)``), all rounded once to bf16 (float32 arrays on the bf16 grid).
+    Slots ``prefix_len[r] + count[r]`` and beyond, which no query may read,
+    hold NaN, so that a read past the admitted slots cannot go unnoticed.
+    Query rows at or past ``count[r]`` are drawn like the others.
+    A larger ``q_scale`` sharpens the attention rows.
+    """
+    q = round_to_bf16(rng.normal(0.0, q_scale, size=(R, N, Hq, D)))
+    k = round_to_bf16(rng.normal(0.0, 1.0, size=(R, Hkv, capacity, D)))
+    v = round_to_bf16(rng.normal(0.0, 1.0, size=(R, Hkv, capacity, D)))
+    for r in range(R):
+        end = int(prefix_len[r]) + int(count[r])
+        k[r, :, end:] = np.nan
+        v[r, :, end:] = np.nan
+    return {"q": q, "k": k, "v": v}
