@@ -221,6 +221,49 @@ pctree_status pctree_compact_kv(void* cache, int64_t request_stride, int64_t gro
                                 const int32_t* accept_len, int32_t requests, int32_t budget,
                                 int32_t max_depth, void* stream);
 
+/* ---------------------------------------------------------------------
+ * Tree-masked verification attention (Sec. 4.2: the packed tree is verified
+ * in one target forward; App. A, "Tensor implementation": a node attends to
+ * the verified prefix, itself and its root-to-node ancestors).  One
+ * attention layer of the target, grouped-query heads, bf16 operands, fp32
+ * accumulation and softmax, bf16 output.
+ * --------------------------------------------------------------------- */
+
+typedef struct pctree_attn_shape {
+  int32_t requests; /* R                                                        */
+  int32_t budget;   /* N: tree rows per request, as emitted by the builder      */
+  int32_t q_heads;  /* Hq                                                       */
+  int32_t kv_heads; /* Hkv, a divisor of Hq; query head h reads kv head h/(Hq/Hkv) */
+  int32_t head_dim; /* D: 64 or 128                                             */
+  int32_t capacity; /* C: cache slots per request and kv head                   */
+  float scale;      /* softmax scale of q.k, usually 1/sqrt(D)                  */
+} pctree_attn_shape;
+
+/* Workspace bytes pctree_tree_attention needs for `shape` (0: none, or an
+ * invalid shape).  Pure host arithmetic. */
+size_t pctree_attention_workspace_bytes(const pctree_attn_shape* shape);
+
+/* out[r][i][h] = sum_s softmax_s(scale * q[r][i][h] . k[r][h/g][s]) v[r][h/g][s]
+ * over the admitted slots s of tree node i: the prefix [0, prefix_len[r]) and
+ * prefix_len[r] + j for every bit j < count[r] set in mask row i (cache slot
+ * prefix_len + j holds tree node j, as after pctree_compact_kv's layout).
+ * q [R][N][Hq][D], k_cache and v_cache [R][Hkv][C][D], out [R][N][Hq][D],
+ * all bf16 (uint16 bits), 16-byte aligned; mask [R][N][(N+31)/32] as from
+ * pctree_build_mask; count [R], prefix_len [R] int32 device arrays.
+ * Rows i >= count[r], and rows that admit no slot, are zero.  prefix_len
+ * and count are clamped to [0, C] and [0, N], and slots at or past C are
+ * never read; slots at or past prefix_len + count are never read either,
+ * so they may hold anything.  Admitted slots must hold finite values.
+ * Errors: INVALID_ARGUMENT (null or misaligned pointer, size < 1, Hq not a
+ * multiple of Hkv, non-finite scale), UNSUPPORTED (D not 64 or 128,
+ * N > PCTREE_MAX_MASK_BUDGET, R or Hkv > 65535, sizes past the index range),
+ * WORKSPACE (a needed workspace null, too small or not 256-byte aligned). */
+pctree_status pctree_tree_attention(const pctree_attn_shape* shape, const void* q,
+                                    const void* k_cache, const void* v_cache,
+                                    const uint32_t* mask, const int32_t* count,
+                                    const int32_t* prefix_len, void* out, void* workspace,
+                                    size_t workspace_bytes, void* stream);
+
 /* Static, human-readable name of a status code. */
 const char* pctree_status_string(pctree_status status);
 

@@ -11,7 +11,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libpctree.so")
-SOURCES = ["pctree_api.hip", "pctree_kernels.hip", "pctree_profile.hip", "pctree_verify.hip"]
+SOURCES = ["pctree_api.hip", "pctree_kernels.hip", "pctree_profile.hip", "pctree_verify.hip",
+           "pctree_attention.hip"]
 ARCH = "gfx950"
 
 

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 
+#include "pctree_attention.h"
 #include "pctree_plan.h"
 #include "pctree_verify.h"
 
@@ -47,6 +48,36 @@ pctree_status check_inputs(const pctree_inputs* in) {
       !aligned(in->depth_feat, 16) || !aligned(in->root_token, 4) || !aligned(in->prefix_len, 4))
     return PCTREE_ERR_INVALID_ARGUMENT;
   return PCTREE_OK;
+}
+
+// Tree attention: shape checks and the work split.  The split is planned for
+// the 256 compute units of the gfx950 part, so that the workspace size is a
+// function of the shape alone.
+constexpr int kAttnPlanCUs = 256;
+
+pctree_status check_attn_shape(const pctree_attn_shape* s) {
+  if (!s) return PCTREE_ERR_INVALID_ARGUMENT;
+  if (s->requests < 1 || s->budget < 1 || s->q_heads < 1 || s->kv_heads < 1 ||
+      s->head_dim < 1 || s->capacity < 1)
+    return PCTREE_ERR_INVALID_ARGUMENT;
+  if (s->q_heads % s->kv_heads != 0) return PCTREE_ERR_INVALID_ARGUMENT;
+  if (!(s->scale == s->scale) || s->scale > 3.4e38f || s->scale < -3.4e38f)
+    return PCTREE_ERR_INVALID_ARGUMENT;  // NaN or infinite scale
+  if (s->head_dim != 64 && s->head_dim != 128) return PCTREE_ERR_UNSUPPORTED;
+  if (s->budget > PCTREE_MAX_MASK_BUDGET || s->requests > 65535 || s->kv_heads > 65535)
+    return PCTREE_ERR_UNSUPPORTED;
+  // element counts of q / out and of one cache tensor stay far inside size_t
+  // and the grid's x extent (query blocks x splits) inside int
+  const long long rows = (long long)s->requests * s->budget * s->q_heads;
+  const long long slots = (long long)s->requests * s->kv_heads * s->capacity;
+  if (rows > (1LL << 31) / s->head_dim || slots > (1LL << 40) / s->head_dim)
+    return PCTREE_ERR_UNSUPPORTED;
+  return PCTREE_OK;
+}
+
+AttnPlan attn_plan(const pctree_attn_shape* s) {
+  return plan_attention(s->requests, s->budget, s->q_heads, s->kv_heads, s->head_dim,
+                        s->capacity, kAttnPlanCUs);
 }
 
 // Chain decode runs the tree builder with k = 1 and N = B + 1; its tree
@@ -321,6 +352,59 @@ pctree_status pctree_compact_kv(void* cache, int64_t request_stride, int64_t gro
     const hipError_t e = launch_compact(cache, request_stride, group_stride, groups, capacity,
                                         slot_bytes, prefix_len, accept_node, accept_len, requests,
                                         budget, max_depth + 1, (hipStream_t)stream);
+    return e == hipSuccess ? PCTREE_OK : PCTREE_ERR_HIP;
+  } catch (...) {
+    return PCTREE_ERR_HIP;
+  }
+}
+
+size_t pctree_attention_workspace_bytes(const pctree_attn_shape* shape) {
+  if (check_attn_shape(shape) != PCTREE_OK) return 0;
+  return attn_plan(shape).ws_bytes;
+}
+
+pctree_status pctree_tree_attention(const pctree_attn_shape* shape, const void* q,
+                                    const void* k_cache, const void* v_cache,
+                                    const uint32_t* mask, const int32_t* count,
+                                    const int32_t* prefix_len, void* out, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  try {
+    const pctree_status st = check_attn_shape(shape);
+    if (st != PCTREE_OK) return st;
+    if (!q || !k_cache || !v_cache || !mask || !count || !prefix_len || !out)
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
+        !aligned(mask, 4) || !aligned(count, 4) || !aligned(prefix_len, 4))
+      return PCTREE_ERR_INVALID_ARGUMENT;
+    const AttnPlan plan = attn_plan(shape);
+    if (plan.ws_bytes > 0 &&
+        (!workspace || !aligned(workspace, 256) || workspace_bytes < plan.ws_bytes))
+      return PCTREE_ERR_WORKSPACE;
+    AttnArgs a;
+    a.q = (const uint16_t*)q;
+    a.k = (const uint16_t*)k_cache;
+    a.v = (const uint16_t*)v_cache;
+    a.mask = mask;
+    a.count = count;
+    a.prefix_len = prefix_len;
+    a.out = (uint16_t*)out;
+    a.R = shape->requests;
+    a.N = shape->budget;
+    a.Hq = shape->q_heads;
+    a.Hkv = shape->kv_heads;
+    a.C = shape->capacity;
+    a.NW = (shape->budget + 31) / 32;
+    a.g = shape->q_heads / shape->kv_heads;
+    a.qblocks = plan.qblocks;
+    a.nsplit = plan.nsplit;
+    a.split_keys = plan.split_keys;
+    a.scale_log2 = shape->scale * 1.4426950408889634f;
+    const size_t rows = (size_t)a.R * a.N * a.Hq;
+    a.part_o = plan.nsplit > 1 ? (float*)workspace : nullptr;
+    a.part_ml = plan.nsplit > 1 ? (float*)workspace + (size_t)plan.nsplit * rows * shape->head_dim
+                                : nullptr;
+    (void)hipGetLastError();
+    const hipError_t e = launch_attention(a, shape->head_dim, (hipStream_t)stream);
     return e == hipSuccess ? PCTREE_OK : PCTREE_ERR_HIP;
   } catch (...) {
     return PCTREE_ERR_HIP;

@@ -22,6 +22,10 @@ __all__ = [
     "build_retrieve",
     "accept_greedy",
     "compact_kv",
+    "AttnShape",
+    "attention_workspace_bytes",
+    "tree_attention",
+    "TreeAttention",
     "TreeBuilder",
     "status_string",
     "F32",
@@ -48,6 +52,12 @@ class PCTreeError(RuntimeError):
 class Shape(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("vocab", "block", "budget", "topk", "rank", "requests", "dtype", "mode")]
+
+
+class AttnShape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("requests", "budget", "q_heads", "kv_heads", "head_dim", "capacity")] + \
+               [("scale", ctypes.c_float)]
 
 
 class _Inputs(ctypes.Structure):
@@ -95,6 +105,11 @@ def lib() -> ctypes.CDLL:
         L.pctree_compact_kv.argtypes = [vp, i64, i64, i32, i32, i32, vp, vp, vp, i32, i32, i32,
                                         vp]
         L.pctree_compact_kv.restype = ctypes.c_int
+        L.pctree_attention_workspace_bytes.argtypes = [ctypes.POINTER(AttnShape)]
+        L.pctree_attention_workspace_bytes.restype = sz
+        L.pctree_tree_attention.argtypes = [ctypes.POINTER(AttnShape), vp, vp, vp, vp, vp, vp, vp,
+                                            vp, sz, vp]
+        L.pctree_tree_attention.restype = ctypes.c_int
         L.pctree_status_string.argtypes = [ctypes.c_int]
         L.pctree_status_string.restype = ctypes.c_char_p
         L.pctree_abi_version.argtypes = []
@@ -324,6 +339,56 @@ def compact_kv(cache, prefix_len, accept_node, accept_len, budget, stream=None):
                                  budget, accept_node.shape[1] - 1, _stream(stream))
     _check(st, "pctree_compact_kv")
     return cache
+
+
+def attention_workspace_bytes(R, N, Hq, Hkv, D, C, scale=None) -> int:
+    sc = float(scale) if scale is not None else D ** -0.5
+    return int(lib().pctree_attention_workspace_bytes(ctypes.byref(
+        AttnShape(R, N, Hq, Hkv, D, C, sc))))
+
+
+class TreeAttention:
+    """One tree-attention layer shape with its workspace, for repeated calls."""
+
+    def __init__(self, R, N, Hq, Hkv, D, C, scale=None, device="cuda"):
+        self.shape = AttnShape(R, N, Hq, Hkv, D, C,
+                               float(scale) if scale is not None else D ** -0.5)
+        nb = int(lib().pctree_attention_workspace_bytes(ctypes.byref(self.shape)))
+        self.workspace = torch.empty(max(nb, 1), dtype=torch.uint8, device=device)
+        self.ws_bytes = nb
+        self.device = device
+
+    def __call__(self, q, k, v, mask, count, prefix_len, out=None, stream=None):
+        s = self.shape
+        R, N, Hq, Hkv, D, C = s.requests, s.budget, s.q_heads, s.kv_heads, s.head_dim, s.capacity
+        for name, t, shp in (("q", q, (R, N, Hq, D)), ("k", k, (R, Hkv, C, D)),
+                             ("v", v, (R, Hkv, C, D))):
+            if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous() \
+                    or tuple(t.shape) != shp:
+                raise ValueError(f"{name} must be a contiguous bf16 device tensor {shp}")
+        if mask.dtype != torch.int32 and mask.dtype != torch.uint32:
+            raise TypeError("mask must be the [R][N][(N+31)/32] words of build_mask")
+        if tuple(mask.shape) != (R, N, (N + 31) // 32) or not mask.is_contiguous() \
+                or not mask.is_cuda:
+            raise ValueError("mask must be [R][N][(N+31)/32] and contiguous")
+        _int32_dev("count", count)
+        _int32_dev("prefix_len", prefix_len)
+        if out is None:
+            out = torch.empty(R, N, Hq, D, dtype=torch.bfloat16, device=q.device)
+        st = lib().pctree_tree_attention(ctypes.byref(s), _ptr(q), _ptr(k), _ptr(v), _ptr(mask),
+                                         _ptr(count), _ptr(prefix_len), _ptr(out),
+                                         _ptr(self.workspace), self.ws_bytes, _stream(stream))
+        _check(st, "pctree_tree_attention")
+        return out
+
+
+def tree_attention(q, k, v, mask, count, prefix_len, scale=None, stream=None):
+    """Tree-masked attention of one target layer: q [R][N][Hq][D], k and v
+    [R][Hkv][C][D] bf16, mask from ``build_mask``; returns out [R][N][Hq][D] bf16."""
+    R, N, Hq, D = q.shape
+    Hkv, C = k.shape[1], k.shape[2]
+    return TreeAttention(R, N, Hq, Hkv, D, C, scale, device=q.device)(
+        q, k, v, mask, count, prefix_len, stream=stream)
 
 
 def device_inputs(inp: dict, device="cuda") -> dict:
