@@ -145,11 +145,64 @@ def time_verify(P, builder, w, inp, reps=200):
     us_r = _event_us(lambda: L.pctree_build_retrieve(*ra), reps)
     us_a = _event_us(lambda: L.pctree_accept_greedy(*aa), reps)
     us_c = _event_us(lambda: L.pctree_compact_kv(*ca), reps)
+    attn = time_attention(P, out, w, prefix, reps)
     return {"retrieve_us": us_r, "accept_us": us_a, "compact_us": us_c,
             "accept_len": [int(x) for x in a_len], "nrows": [int(x) for x in nrows.cpu()],
             "compact_bytes": 2 * moved * groups * slot * 2,
             "kv": "72 groups (36 layers x K/V) x 8 heads x 128 dims bf16 per slot",
-            "target": "synthetic: a child's token with p = 0.8 at each node, else uniform"}
+            "target": "synthetic: a child's token with p = 0.8 at each node, else uniform",
+            "attention": attn}
+
+
+def time_attention(P, out, w, prefix, reps):
+    """One tree-masked attention layer of the target's verification forward on
+    the round's own tree: Qwen3 attention shapes (32 query / 8 key-value heads,
+    or 40 / 8 for the 14B batch), head dimension 128, bf16, over each
+    request's prefix and tree slots."""
+    import ctypes
+
+    import numpy as np
+    import torch
+    from paper_2608_02123_amd import synth
+
+    Hq, Hkv, D = synth.ATTN_SHAPES["qwen3_14b" if w.R > 1 else "qwen3_4b"]
+    cnt = out["count"].cpu().numpy().astype(np.int64)
+    pre = np.asarray(prefix, dtype=np.int64)
+    C = int((pre + w.N).max())
+    t = synth.make_attention_inputs(np.random.default_rng(3), w.R, w.N, Hq, Hkv, D, pre, cnt, C)
+    t["k"] = np.nan_to_num(t["k"])  # slots nobody reads: zeros rather than NaN
+    t["v"] = np.nan_to_num(t["v"])
+
+    def up(a):
+        return torch.from_numpy(synth.bf16_bits(a).view(np.int16)).cuda().view(torch.bfloat16)
+
+    q, k, v = up(t["q"]), up(t["k"]), up(t["v"])
+    att = P.TreeAttention(w.R, w.N, Hq, Hkv, D, C, D ** -0.5)
+    pre_d = torch.from_numpy(pre.astype(np.int32)).cuda()
+    res = att(q, k, v, out["mask"], out["count"], pre_d)
+    torch.cuda.synchronize()
+    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    vp = lambda x: ctypes.c_void_p(x.data_ptr())  # noqa: E731
+    args = (ctypes.byref(att.shape), vp(q), vp(k), vp(v), vp(out["mask"]), vp(out["count"]),
+            vp(pre_d), vp(res), vp(att.workspace), att.ws_bytes, st)
+    L = P.lib()
+    us = _event_us(lambda: L.pctree_tree_attention(*args), reps)
+    # algorithmic traffic: each admitted range of K and V read once per kv head,
+    # the queries read and the outputs written once
+    slots = int((pre + cnt).sum())
+    nodes = int(cnt.sum())
+    bytes_ = 2 * Hkv * slots * D * 2 + 2 * nodes * Hq * D * 2
+    # flops: q.k and p.v over every admitted slot of every (node, head)
+    mask = out["mask"].cpu().numpy().view(np.uint32)
+    tree_adm = sum(int(sum(bin(int(x)).count("1") for x in mask[r, :cnt[r]].ravel()))
+                   for r in range(w.R))
+    adm = int(sum(pre[r] * cnt[r] for r in range(w.R))) + tree_adm
+    flops = 4 * adm * Hq * D
+    return {"us": us, "heads": f"{Hq}/{Hkv}x{D}", "capacity": C,
+            "algorithmic_bytes": bytes_, "gbs": bytes_ / us / 1e3,
+            "hbm_frac": bytes_ / us / 1e3 / HBM_PEAK_GBS,
+            "flops": flops, "tflops": flops / us / 1e6, "mfma_frac": flops / us / 1e6 / 2500.0,
+            "splits": att.ws_bytes > 0}
 
 
 def time_sweeps(P, w, inp, dev, reps=30):

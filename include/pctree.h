@@ -236,7 +236,7 @@ typedef struct pctree_attn_shape {
   int32_t kv_heads; /* Hkv, a divisor of Hq; query head h reads kv head h/(Hq/Hkv) */
   int32_t head_dim; /* D: 64 or 128                                             */
   int32_t capacity; /* C: cache slots per request and kv head                   */
-  float scale;      /* softmax scale of q.k, usually 1/sqrt(D)                  */
+  float scale;      /* softmax scale of q.k, > 0, usually 1/sqrt(D)             */
 } pctree_attn_shape;
 
 /* Workspace bytes pctree_tree_attention needs for `shape` (0: none, or an
@@ -255,7 +255,7 @@ size_t pctree_attention_workspace_bytes(const pctree_attn_shape* shape);
  * never read; slots at or past prefix_len + count are never read either,
  * so they may hold anything.  Admitted slots must hold finite values.
  * Errors: INVALID_ARGUMENT (null or misaligned pointer, size < 1, Hq not a
- * multiple of Hkv, non-finite scale), UNSUPPORTED (D not 64 or 128,
+ * multiple of Hkv, scale not positive and finite), UNSUPPORTED (D not 64 or 128,
  * N > PCTREE_MAX_MASK_BUDGET, R or Hkv > 65535, sizes past the index range),
  * WORKSPACE (a needed workspace null, too small or not 256-byte aligned). */
 pctree_status pctree_tree_attention(const pctree_attn_shape* shape, const void* q,

@@ -61,13 +61,13 @@ pctree_status check_attn_shape(const pctree_attn_shape* s) {
       s->head_dim < 1 || s->capacity < 1)
     return PCTREE_ERR_INVALID_ARGUMENT;
   if (s->q_heads % s->kv_heads != 0) return PCTREE_ERR_INVALID_ARGUMENT;
-  if (!(s->scale == s->scale) || s->scale > 3.4e38f || s->scale < -3.4e38f)
-    return PCTREE_ERR_INVALID_ARGUMENT;  // NaN or infinite scale
+  if (!(s->scale > 0.0f) || s->scale > 3.4e38f)
+    return PCTREE_ERR_INVALID_ARGUMENT;  // scale not positive and finite
   if (s->head_dim != 64 && s->head_dim != 128) return PCTREE_ERR_UNSUPPORTED;
   if (s->budget > PCTREE_MAX_MASK_BUDGET || s->requests > 65535 || s->kv_heads > 65535)
     return PCTREE_ERR_UNSUPPORTED;
-  // element counts of q / out and of one cache tensor stay far inside size_t
-  // and the grid's x extent (query blocks x splits) inside int
+  // element counts of q / out and of one cache tensor stay far inside size_t,
+  // and the grid (groups x query blocks, padded to whole XCD rounds) inside int
   const long long rows = (long long)s->requests * s->budget * s->q_heads;
   const long long slots = (long long)s->requests * s->kv_heads * s->capacity;
   if (rows > (1LL << 31) / s->head_dim || slots > (1LL << 40) / s->head_dim)
@@ -404,7 +404,7 @@ pctree_status pctree_tree_attention(const pctree_attn_shape* shape, const void* 
     a.part_ml = plan.nsplit > 1 ? (float*)workspace + (size_t)plan.nsplit * rows * shape->head_dim
                                 : nullptr;
     (void)hipGetLastError();
-    const hipError_t e = launch_attention(a, shape->head_dim, (hipStream_t)stream);
+    const hipError_t e = launch_attention(a, plan.blocks, shape->head_dim, (hipStream_t)stream);
     return e == hipSuccess ? PCTREE_OK : PCTREE_ERR_HIP;
   } catch (...) {
     return PCTREE_ERR_HIP;

@@ -13,7 +13,8 @@ namespace pctree {
 struct AttnPlan {
   int qblocks;      // 64-row query blocks per (request, key/value head)
   int nsplit;       // key-slot runs per query block (1: no merge pass)
-  int split_keys;   // slots per run, a multiple of 32
+  int split_keys;   // slots per run, a multiple of 64
+  int blocks;       // workgroups of the attention kernel (XCD-grouped, padded)
   size_t ws_bytes;  // workspace of the merge pass (0 when nsplit == 1)
 };
 
@@ -26,14 +27,14 @@ struct AttnArgs {
   const int* prefix_len;  // [R]
   uint16_t* out;          // [R][N][Hq][D] bf16
   float* part_o;          // [nsplit][R][N][Hq][D] (split runs only)
-  float* part_ml;         // [nsplit][R][N][Hq][2] (max in base 2, sum)
+  float* part_ml;         // [nsplit][R][N][Hq][2] (max of q.k, sum of weights)
   int R, N, Hq, Hkv, C, NW, g;
   int qblocks, nsplit, split_keys;
-  float scale_log2;       // softmax scale times log2(e)
+  float scale_log2;       // softmax scale times log2(e), > 0
 };
 
 AttnPlan plan_attention(int R, int N, int Hq, int Hkv, int D, int C, int cus);
 
-hipError_t launch_attention(AttnArgs a, int D, hipStream_t stream);
+hipError_t launch_attention(AttnArgs a, int blocks, int D, hipStream_t stream);
 
 }  // namespace pctree

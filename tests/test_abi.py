@@ -209,12 +209,12 @@ def _attn_shape(R=1, N=64, Hq=32, Hkv=8, D=128, C=1088, scale=None):
 
 def test_tree_attention_workspace():
     ws = lambda **kw: P.lib().pctree_attention_workspace_bytes(ctypes.byref(_attn_shape(**kw)))  # noqa: E731,E501
-    # few workgroups (one request, 8 kv heads, 4 query blocks): the slots are split
-    # into 12 runs of 96, each leaving D + 2 floats per (node, head)
-    assert ws() == 12 * 64 * 32 * (128 + 2) * 4 + 256
+    # few workgroups (one request, 8 kv heads, 2 query blocks): the 1088 slots are
+    # split into 9 runs of 128, each leaving D + 2 floats per (node, head)
+    assert ws() == 9 * 64 * 32 * (128 + 2) * 4 + 256
     # enough workgroups without a split: no workspace
     assert ws(R=8, N=128, Hq=40) == 0
-    assert ws(C=20) == 0  # a single 32-slot chunk cannot be split
+    assert ws(C=64) == 0  # a single 64-slot chunk is not split
     for bad in (dict(R=0), dict(N=0), dict(Hq=0), dict(Hkv=0), dict(D=0), dict(C=0),
                 dict(Hq=30), dict(D=96), dict(N=1025), dict(scale=float("nan")),
                 dict(scale=float("inf"))):
@@ -236,7 +236,8 @@ def test_tree_attention_validation():
         assert call(ptrs=p) == P.ERR_INVALID_ARGUMENT, i
         p[i] = A + (8 if i in (0, 1, 2, 6) else 2)
         assert call(ptrs=p) == P.ERR_INVALID_ARGUMENT, i
-    for kw in (dict(R=0), dict(Hq=12, Hkv=8), dict(scale=float("nan")), dict(C=-1)):
+    for kw in (dict(R=0), dict(Hq=12, Hkv=8), dict(scale=float("nan")), dict(C=-1),
+               dict(scale=0.0), dict(scale=-0.125)):
         assert call(shape=_attn_shape(**kw)) == P.ERR_INVALID_ARGUMENT, kw
     for kw in (dict(D=96), dict(N=1025), dict(R=70000)):
         assert call(shape=_attn_shape(**kw)) == P.ERR_UNSUPPORTED, kw

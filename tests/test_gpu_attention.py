@@ -173,3 +173,14 @@ def test_repeated_calls_reuse_the_workspace():
                   P.build_mask(par, cnt), cnt, _i32_dev(c["prefix"]))
         torch.cuda.synchronize()
         _compare(c, out.float().cpu().numpy(), _oracle(c, scale), "repeat")
+
+
+def test_wide_tree_one_head_per_group():
+    """g = 1 (one query head per kv head) with a 300-node tree after a
+    1500-slot prefix: 64 nodes per workgroup, tree slots spread over several
+    mask words and slot runs."""
+    c = _case(8, 1, 300, 8, 8, 128, [1500], [300], max_depth=40)
+    scale = 128 ** -0.5
+    gpu, att = _run_gpu(c, scale)
+    assert att.ws_bytes > 0
+    _compare(c, gpu, _oracle(c, scale), "wide")
