@@ -1833,6 +1833,7 @@ __device__ void select_tail(const Plan& p, int d, int P, int req, SelShared& ssh
 // multi-launch form, wide frontiers (more than 16 rows per stage)
 // ---------------------------------------------------------------------------
 constexpr int kWideWaves = 8;      // column blocks of 16 rows one workgroup serves
+constexpr int kWideAhead = 3;      // W tiles in flight per workgroup beyond the one in LDS
 constexpr int kMergeThreads = 256;
 
 // Publish one wave's rows (column block) of a slice: the four lanes of a row
@@ -1894,45 +1895,64 @@ __global__ __launch_bounds__(kWideWaves * 64) void head_wide_kernel(Plan p, int 
   // lane l fetches what lane l of a consumer feeds the MFMA: token l % 16 of
   // the tile (clamped into the vocabulary), rank group l / 16; chunks past
   // the rank re-read the last one (finite values that meet zero B fragments)
-  u32x4 stage[CPW];
-  auto fetch = [&](int t) {
+  auto fetch = [&](int t, u32x4 (&dst)[CPW]) {
     const int tok = min(t * kTile + (lane & 15), p.V - 1);
     const char* wrow = (const char*)p.Wt + ((size_t)tok * p.r + (lane >> 4) * (KC / 4)) * ESZ;
 #pragma unroll
     for (int q = 0; q < CPW; ++q) {
       const int c = wave + q * kWideWaves;
-      if (c < NCMAX) stage[q] = *(const u32x4*)(wrow + (size_t)min(c, p.nchunk - 1) * KC * ESZ);
+      if (c < NCMAX) dst[q] = *(const u32x4*)(wrow + (size_t)min(c, p.nchunk - 1) * KC * ESZ);
     }
   };
-  auto put = [&](int buf) {
+  auto put = [&](int buf, const u32x4 (&src)[CPW]) {
 #pragma unroll
     for (int q = 0; q < CPW; ++q) {
       const int c = wave + q * kWideWaves;
-      if (c < NCMAX) tiles[buf][c][lane] = stage[q];
+      if (c < NCMAX) tiles[buf][c][lane] = src[q];
     }
   };
-  uint32_t l[4] = {0u, 0u, 0u, 0u}, ln[4] = {0u, 0u, 0u, 0u};
-  fetch(t0);
+  // Tile t is computed from LDS buffer (t - t0) & 1 while tiles t + 1 ..
+  // t + kWideAhead are in flight in register slots: tile t0 + 1 + i + n
+  // kWideAhead sits in slot i (a W tile is 16 KB per workgroup, so one tile
+  // ahead would leave the memory system far from its bandwidth-latency
+  // product).
+  u32x4 stg[kWideAhead][CPW];
+  uint32_t lf[kWideAhead][4];
+  uint32_t l[4] = {0u, 0u, 0u, 0u};
+  fetch(t0, stg[0]);
   if (live) load_lfrag<DT>(p, h, d, t0, l);
-  put(0);
+  put(0, stg[0]);
+#pragma unroll
+  for (int i = 0; i < kWideAhead; ++i) {
+    if (t0 + 1 + i < t1) {
+      fetch(t0 + 1 + i, stg[i]);
+      if (live) load_lfrag<DT>(p, h, d, t0 + 1 + i, lf[i]);
+    }
+  }
   __syncthreads();
-  for (int t = t0; t < t1; ++t) {
-    const int buf = (t - t0) & 1;
-    const bool more = t + 1 < t1;
-    if (more) {
-      fetch(t + 1);
-      if (live) load_lfrag<DT>(p, h, d, t + 1, ln);
-    }
-    if (live) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int tb = t0; tb < t1; tb += kWideAhead) {
 #pragma unroll
-      for (int c = 0; c < NCMAX; ++c) acc = mfma_chunk<DT>(tiles[buf][c][lane], bfrag[c], acc);
-      tile_epilogue<DT, KMAX>(p, h, acc, l, t, h.row_ok, r);
-    }
-    if (more) put(buf ^ 1);
+    for (int i = 0; i < kWideAhead; ++i) {
+      const int t = tb + i;
+      if (t >= t1) break;
+      const int buf = (t - t0) & 1;
+      if (live) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) l[i] = ln[i];
-    __syncthreads();
+        for (int c = 0; c < NCMAX; ++c) acc = mfma_chunk<DT>(tiles[buf][c][lane], bfrag[c], acc);
+        tile_epilogue<DT, KMAX>(p, h, acc, l, t, h.row_ok, r);
+      }
+      if (t + 1 < t1) {
+        put(buf ^ 1, stg[i]);  // tile t + 1
+#pragma unroll
+        for (int e = 0; e < 4; ++e) l[e] = lf[i][e];
+      }
+      if (t + 1 + kWideAhead < t1) {
+        fetch(t + 1 + kWideAhead, stg[i]);
+        if (live) load_lfrag<DT>(p, h, d, t + 1 + kWideAhead, lf[i]);
+      }
+      __syncthreads();
+    }
   }
   if (live) publish_wave<KMAX>(p, h, slice, r);
 }
