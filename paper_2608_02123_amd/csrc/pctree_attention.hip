@@ -50,6 +50,7 @@ constexpr int kVPad = 8;           // bf16 padding of an LDS V^T row
 constexpr int kMaxSplits = 32;     // slot runs merged by one merge thread
 constexpr int kXcds = 8;           // L2 domains the dispatcher deals workgroups over
 constexpr int kMergeThreads = 256;
+constexpr int kMergeBatch = 8;     // slot runs whose loads one merge thread issues together
 constexpr float kNegInf = -__builtin_inff();
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -418,11 +419,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 }
 
 // Merge of the slot runs: D / 4 threads per row of (request, node, head), 4
-// consecutive d each.  Only the runs that hold admitted slots were written;
-// every load of a thread is issued before the first is used.
+// consecutive d each.  Only the runs that hold admitted slots were written.
+// The runs are read in batches of kMergeBatch whose loads are all issued
+// before any is used (clamped to a written run), folded into a running
+// (max, sum, output) per batch.
 template <int D>
 __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a) {
-  constexpr int TPR = D / 4;               // threads per row
+  constexpr int TPR = D / 4;                // threads per row
   constexpr int RPB = kMergeThreads / TPR;  // rows per workgroup
   const size_t rows = (size_t)a.R * a.N * a.Hq;
   const size_t qidx = (size_t)blockIdx.x * RPB + threadIdx.x / TPR;
@@ -432,32 +435,37 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a) {
   const int node = (int)(qidx / a.Hq % a.N);
   const ReqRange rr = req_range(a, r);
   const int ns = node < rr.cnt ? min(a.nsplit, (rr.end + a.split_keys - 1) / a.split_keys) : 0;
-  float ms[kMaxSplits], ls[kMaxSplits];
-  f32x4 os[kMaxSplits];
-#pragma unroll
-  for (int s = 0; s < kMaxSplits; ++s) {
-    if (s < ns) {
-      const size_t prow = (size_t)s * rows + qidx;
-      ms[s] = a.part_ml[2 * prow];
-      ls[s] = a.part_ml[2 * prow + 1];
-      os[s] = *(const f32x4*)(a.part_o + prow * D + d);
-    }
-  }
-  float M = kNegInf;
-#pragma unroll
-  for (int s = 0; s < kMaxSplits; ++s)
-    if (s < ns) M = fmaxf(M, ms[s]);
+  float M = kNegInf, L = 0.0f;
   f32x4 O = {0.f, 0.f, 0.f, 0.f};
-  float L = 0.0f;
-  if (M != kNegInf) {
+  for (int s0 = 0; s0 < ns; s0 += kMergeBatch) {
+    float ms[kMergeBatch], ls[kMergeBatch];
+    f32x4 os[kMergeBatch];
 #pragma unroll
-    for (int s = 0; s < kMaxSplits; ++s) {
-      if (s < ns && ms[s] != kNegInf) {  // a run with no admitted slot of this row adds nothing
-        const float w = exp2_hw((ms[s] - M) * a.scale_log2);  // maxima in raw units
-        L += w * ls[s];
-        O += os[s] * w;
+    for (int i = 0; i < kMergeBatch; ++i) {
+      const size_t prow = (size_t)min(s0 + i, ns - 1) * rows + qidx;
+      ms[i] = a.part_ml[2 * prow];
+      ls[i] = a.part_ml[2 * prow + 1];
+      os[i] = *(const f32x4*)(a.part_o + prow * D + d);
+    }
+    float bm = kNegInf;
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i)
+      if (s0 + i < ns) bm = fmaxf(bm, ms[i]);
+    const float Mn = fmaxf(M, bm);
+    if (Mn == kNegInf) continue;  // no admitted slot so far
+    const float sc = M == kNegInf ? 0.0f : exp2_hw((M - Mn) * a.scale_log2);
+    L *= sc;
+    O *= sc;
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i) {
+      // a run with no admitted slot of this row (max -inf) adds nothing
+      if (s0 + i < ns && ms[i] != kNegInf) {
+        const float w = exp2_hw((ms[i] - Mn) * a.scale_log2);  // maxima in raw units
+        L += w * ls[i];
+        O += os[i] * w;
       }
     }
+    M = Mn;
   }
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
   u32x2 w;
