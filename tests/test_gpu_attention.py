@@ -184,3 +184,37 @@ def test_wide_tree_one_head_per_group():
     gpu, att = _run_gpu(c, scale)
     assert att.ws_bytes > 0
     _compare(c, gpu, _oracle(c, scale), "wide")
+
+
+def test_round_tree_through_attention():
+    """End to end on the GPU: the qwen4b_b16 round's tree and mask (builder),
+    then one Qwen3-4B attention layer over them.  The oracle builds its own
+    tree from the same inputs (not the GPU's) and attends over it; with no
+    near-tie in the round the two trees are identical, so the outputs must
+    agree to the attention tolerance."""
+    from paper_2608_02123_amd.synth import CONFIGS, make_inputs
+
+    P = _lib()
+    w = CONFIGS["qwen4b_b16"]
+    inp = make_inputs(w)
+    ref_tree = O.build_tree_batch(inp, w.k, w.N)[0]
+    out = P.build_tree(**P.device_inputs(inp), k=w.k, N=w.N, mask=True)
+    torch.cuda.synchronize()
+    par_gpu = out["parent"][0].cpu().numpy()
+    assert int(out["count"][0]) == int(ref_tree["count"])
+    np.testing.assert_array_equal(par_gpu, np.asarray(ref_tree["parent"], dtype=np.int32))
+    np.testing.assert_array_equal(out["token"][0].cpu().numpy(),
+                                  np.asarray(ref_tree["token"], dtype=np.int32))
+
+    Hq, Hkv, D = QWEN4B
+    n = int(ref_tree["count"])
+    pre = np.array([int(inp["prefix_len"][0])], np.int32)
+    cnt = np.array([n], np.int32)
+    c = _case(9, 1, w.N, Hq, Hkv, D, pre, cnt)
+    c["parent"][0] = np.asarray(ref_tree["parent"], dtype=np.int32)  # the oracle's tree
+    scale = D ** -0.5
+    att = P.TreeAttention(1, w.N, Hq, Hkv, D, c["C"], scale)
+    gpu = att(_bf16_dev(c["q"]), _bf16_dev(c["k"]), _bf16_dev(c["v"]), out["mask"],
+              out["count"], _i32_dev(pre))  # the GPU's own mask and count
+    torch.cuda.synchronize()
+    _compare(c, gpu.float().cpu().numpy(), _oracle(c, scale), "round tree")
