@@ -218,3 +218,13 @@ def test_round_tree_through_attention():
               out["count"], _i32_dev(pre))  # the GPU's own mask and count
     torch.cuda.synchronize()
     _compare(c, gpu.float().cpu().numpy(), _oracle(c, scale), "round tree")
+
+
+def test_max_budget_tree():
+    """The largest tree the mask allows (N = 1024, 32 mask words per row), one
+    head per group, D = 64, after a 700-slot prefix, in two requests (one
+    with a partial tree)."""
+    c = _case(10, 2, 1024, 2, 2, 64, [700, 33], [1024, 517], max_depth=63)
+    scale = 64 ** -0.5
+    gpu, _ = _run_gpu(c, scale)
+    _compare(c, gpu, _oracle(c, scale), "max budget")
