@@ -482,9 +482,11 @@ AttnPlan plan_attention(int R, int N, int Hq, int Hkv, int D, int C, int cus) {
   p.qblocks = (N * g + kRowsPerBlock - 1) / kRowsPerBlock;
   const long long base = (long long)R * Hkv * p.qblocks;
   const int chunks = (C + kChunk - 1) / kChunk;
-  // enough workgroups for one per compute unit
+  // enough workgroups for one per two compute units (more runs cost more in
+  // the merge pass than they save here)
   int ns = 1;
-  if (base < cus) ns = (int)((cus + base - 1) / base);
+  const int target = cus / 2;
+  if (base < target) ns = (int)((target + base - 1) / base);
   ns = ns < chunks ? ns : chunks;
   ns = ns < kMaxSplits ? ns : kMaxSplits;
   ns = ns < 1 ? 1 : ns;

@@ -210,8 +210,8 @@ def _attn_shape(R=1, N=64, Hq=32, Hkv=8, D=128, C=1088, scale=None):
 def test_tree_attention_workspace():
     ws = lambda **kw: P.lib().pctree_attention_workspace_bytes(ctypes.byref(_attn_shape(**kw)))  # noqa: E731,E501
     # few workgroups (one request, 8 kv heads, 2 query blocks): the 1088 slots are
-    # split into 9 runs of 128, each leaving D + 2 floats per (node, head)
-    assert ws() == 9 * 64 * 32 * (128 + 2) * 4 + 256
+    # split into 6 runs of 192, each leaving D + 2 floats per (node, head)
+    assert ws() == 6 * 64 * 32 * (128 + 2) * 4 + 256
     # enough workgroups without a split: no workspace
     assert ws(R=8, N=128, Hq=40) == 0
     assert ws(C=64) == 0  # a single 64-slot chunk is not split
