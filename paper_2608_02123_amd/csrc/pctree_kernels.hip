@@ -1608,38 +1608,61 @@ __device__ void mask_rows(const int* par, int count, int N, uint32_t* out, uint3
 }
 
 // Canonical order: depth ascending, then (parent's emitted index, token).
-// Level by level, every node of the level ranks itself among its level.
-// Uses threads [0, 256) of the block (N <= 256); all threads must call it.
+// Level by level, every node of the level ranks itself among its level by
+// the key (emitted index of its parent + 1) << 20 | token, written to a
+// dense slot of the level (tokens < 2^20, indices < 2^11).  Each node finds
+// its parent among the selected nodes of the level above once, up front.
+// The global reads (the request's flags and the selected nodes' pool
+// entries) are issued together, and the LDS loops issue their reads in
+// batches of 8 (a dependent LDS read per step would cost its full latency
+// every time).  The ancestor mask row of a node is its parent's row (done a
+// level earlier) plus its own bit.  Uses threads [0, 256) of the block
+// (N <= 256); all threads must call it.
 __device__ void emit_request(const Plan& p, const State& st, int req) {
-  __shared__ int sh_node[kEmitThreads], sh_emit[kEmitThreads], sh_par_emit[kEmitThreads];
-  __shared__ uint64_t sh_skey[kEmitThreads];
-  __shared__ int lev_cnt[64], lev_off[65], lev_fill[64], lev_mem[kEmitThreads];
-  __shared__ uint32_t sh_words[kEmitThreads * (PCTREE_EMIT_MAX_N / 32)];
+  constexpr int kBatch = 8;
+  __shared__ int sh_node[kEmitThreads], sh_emit[kEmitThreads];
+  __shared__ int sh_td[kEmitThreads];     // depth << 20 | token
+  __shared__ uint32_t sh_lkey[kEmitThreads];  // level keys, by level slot
+  __shared__ int lev_cnt[64], lev_off[65], lev_fill[64];
+  __shared__ int sh_maxdep;
+  __shared__ uint32_t sh_words[kEmitThreads * (PCTREE_EMIT_MAX_N / 32)];  // mask rows
 
   const int tid = threadIdx.x;
   const int kk = p.kk;
   const int pool = 1 + kk + (p.B - 1) * kk * kk;
-  int count = min(p.N, pool);
-  if (p.req_bad[req]) count = 0;
+  const int count0 = min(p.N, pool);
   const size_t pb = (size_t)req * p.maxpool;
+
+  // every global read at once: the request's flags and the pool entries of
+  // the first count0 selected nodes (the top-N ids live in LDS)
+  const int bad = p.req_bad[req];
+  const int prefix = p.prefix[req];
+  int node = -1, dep = -1, tok = -1, pnode = -1;
+  float score = 0.0f;
+  if (tid < count0) {
+    // (clamped: an inconsistent state must not address outside the pool)
+    node = min(max(st.top_node[(size_t)req * p.N + tid], 0), p.maxpool - 1);
+    dep = p.node_depth[pb + node];
+    tok = p.node_tok[pb + node];
+    pnode = p.node_par[pb + node];
+    score = p.node_score[pb + node];
+  }
+  const int count = bad ? 0 : count0;
 
   __syncthreads();
   if (tid < 64) {
     lev_cnt[tid] = 0;
     lev_fill[tid] = 0;
   }
+  if (tid == 0) sh_maxdep = -1;
   __syncthreads();
-  int node = -1, dep = -1, tok = -1, pnode = -1;
-  float score = 0.0f;
-  if (tid < count) {
-    // (clamped: an inconsistent state must not address outside the pool)
-    node = min(max(st.top_node[(size_t)req * p.N + tid], 0), p.maxpool - 1);
-    dep = min(max(p.node_depth[pb + node], 0), p.B);
-    tok = p.node_tok[pb + node];
-    pnode = p.node_par[pb + node];
-    score = p.node_score[pb + node];
+  const bool mine = tid < count;
+  if (mine) {
+    dep = min(max(dep, 0), p.B);
     sh_node[tid] = node;
+    sh_td[tid] = (dep << 20) | (tok & 0xFFFFF);
     atomicAdd(&lev_cnt[dep], 1);
+    atomicMax(&sh_maxdep, dep);
   }
   __syncthreads();
   if (tid == 0) {
@@ -1650,40 +1673,68 @@ __device__ void emit_request(const Plan& p, const State& st, int req) {
     }
     lev_off[p.B + 1] = acc;
   }
-  __syncthreads();
-  if (tid < count) lev_mem[lev_off[dep] + atomicAdd(&lev_fill[dep], 1)] = tid;
-  __syncthreads();
+  // the parent among the selected nodes one level up (-1: none)
+  int pidx = -1;
+  if (mine && dep > 0) {
+    const int want = (dep - 1) << 20;
+    for (int j0 = 0; j0 < count; j0 += kBatch) {
+      int nd[kBatch], td[kBatch];
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        const int j = min(j0 + i, count - 1);
+        nd[i] = sh_node[j];
+        td[i] = sh_td[j];
+      }
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i)
+        if (j0 + i < count && nd[i] == pnode && (td[i] & ~0xFFFFF) == want) pidx = j0 + i;
+    }
+  }
+  __syncthreads();  // lev_off
+  const int myslot = mine ? lev_off[dep] + atomicAdd(&lev_fill[dep], 1) : -1;
 
   int emit = -1, pemit = -1;
-  for (int l = 0; l <= p.B; ++l) {
-    if (dep == l) {
-      if (l > 0) {
-        for (int q = lev_off[l - 1]; q < lev_off[l]; ++q) {
-          const int j = lev_mem[q];
-          if (sh_node[j] == pnode) pemit = sh_emit[j];
-        }
-      }
-      sh_skey[tid] = ((uint64_t)(uint32_t)(pemit + 1) << 32) | (uint32_t)tok;
+  const int maxdep = sh_maxdep;
+  constexpr int MW = PCTREE_EMIT_MAX_N / 32;  // mask words of a row in LDS
+  const int nw = (p.N + 31) / 32;
+  for (int l = 0; l <= maxdep; ++l) {
+    const bool here = mine && dep == l;
+    uint32_t key = 0;
+    if (here) {
+      pemit = pidx >= 0 ? sh_emit[pidx] : -1;
+      key = ((uint32_t)(pemit + 1) << 20) | (uint32_t)(tok & 0xFFFFF);
+      sh_lkey[myslot] = key;
     }
     __syncthreads();
-    if (dep == l) {
-      const uint64_t key = sh_skey[tid];
+    if (here) {
+      const int q0 = lev_off[l], q1 = lev_off[l + 1];
       int rank = 0;
-      for (int q = lev_off[l]; q < lev_off[l + 1]; ++q) rank += sh_skey[lev_mem[q]] < key;
-      emit = lev_off[l] + rank;
+      for (int q = q0; q < q1; q += kBatch) {
+        uint32_t k8[kBatch];
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) k8[i] = sh_lkey[min(q + i, q1 - 1)];
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) rank += (q + i < q1) && k8[i] < key;
+      }
+      emit = q0 + rank;
       sh_emit[tid] = emit;
+      if (p.o_mask) {
+        for (int w = 0; w < nw; ++w) {
+          const uint32_t up = pemit >= 0 ? sh_words[pemit * MW + w] : 0u;
+          sh_words[emit * MW + w] = up | (w == (emit >> 5) ? 1u << (emit & 31) : 0u);
+        }
+      }
     }
     __syncthreads();
   }
 
   const size_t ob = (size_t)req * p.N;
-  if (tid < count) {
+  if (mine) {
     p.o_token[ob + emit] = tok;
     p.o_parent[ob + emit] = pemit;
     p.o_depth[ob + emit] = dep;
-    p.o_position[ob + emit] = p.prefix[req] + dep;
+    p.o_position[ob + emit] = prefix + dep;
     p.o_logprob[ob + emit] = score;
-    sh_par_emit[emit] = pemit;
   }
   for (int e = count + tid; e < p.N; e += blockDim.x) {
     p.o_token[ob + e] = -1;
@@ -1694,10 +1745,9 @@ __device__ void emit_request(const Plan& p, const State& st, int req) {
   }
   if (tid == 0) p.o_count[req] = count;
   if (p.o_mask) {
-    __syncthreads();
-    if (tid < kEmitThreads)
-      mask_rows(sh_par_emit, count, p.N, p.o_mask + (size_t)req * p.N * ((p.N + 31) / 32),
-                sh_words, PCTREE_EMIT_MAX_N / 32);
+    uint32_t* out = p.o_mask + (size_t)req * p.N * nw;
+    for (int e = tid; e < p.N; e += blockDim.x)
+      for (int w = 0; w < nw; ++w) out[(size_t)e * nw + w] = e < count ? sh_words[e * MW + w] : 0u;
   }
   __syncthreads();
 }
