@@ -509,8 +509,10 @@ __global__ __launch_bounds__(kEmitThreads) void prologue_kernel(Plan p) {
 // receives C[token 4*(l/16)+i][row l%16], i = 0..3.
 template <int KMAX, int WAVES>
 struct HeadShared {
-  uint64_t wl[WAVES][kTile][KMAX];
-  uint64_t wt[WAVES][kTile][KMAX < 4 ? KMAX : 4];
+  // key-major, so that the 16 or 64 lanes writing or reading key i of their
+  // rows touch consecutive words (no bank conflicts)
+  uint64_t wl[KMAX][WAVES][kTile];
+  uint64_t wt[KMAX < 4 ? KMAX : 4][WAVES][kTile];
   float2 wms[WAVES][kTile];
 };
 
@@ -776,20 +778,20 @@ __device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h
     lse_combine_pair<32>(m, sum);
     if (h.grp == 0) {
 #pragma unroll
-      for (int i = 0; i < HT; ++i) sh.wt[h.wave][h.col][i] = t[i];
+      for (int i = 0; i < HT; ++i) sh.wt[i][h.wave][h.col] = t[i];
       sh.wms[h.wave][h.col] = make_float2(m, sum);
     }
     __syncthreads();
     if (h.wave == 0) {
 #pragma unroll
-      for (int i = 0; i < HT; ++i) t[i] = sh.wt[h.grp][h.col][i];
+      for (int i = 0; i < HT; ++i) t[i] = sh.wt[i][h.grp][h.col];
       m = sh.wms[h.grp][h.col].x;
       sum = sh.wms[h.grp][h.col].y;
 #pragma unroll
       for (int w = h.grp + 4; w < WAVES; w += 4) {
         uint64_t x[HT];
 #pragma unroll
-        for (int i = 0; i < HT; ++i) x[i] = sh.wt[w][h.col][i];
+        for (int i = 0; i < HT; ++i) x[i] = sh.wt[i][w][h.col];
         list_merge(t, x);
         lse_combine(m, sum, sh.wms[w][h.col].x, sh.wms[w][h.col].y);
       }
@@ -829,17 +831,17 @@ __device__ __forceinline__ void publish_partial(const Plan& p, const HeadLane& h
     list_merge_pair<32>(r.list);
     if (h.grp == 0) {
 #pragma unroll
-      for (int i = 0; i < KMAX; ++i) sh.wl[h.wave][h.col][i] = r.list[i];
+      for (int i = 0; i < KMAX; ++i) sh.wl[i][h.wave][h.col] = r.list[i];
     }
     __syncthreads();
     if (h.wave == 0) {
 #pragma unroll
-      for (int i = 0; i < KMAX; ++i) r.list[i] = sh.wl[h.grp][h.col][i];
+      for (int i = 0; i < KMAX; ++i) r.list[i] = sh.wl[i][h.grp][h.col];
 #pragma unroll
       for (int w = h.grp + 4; w < WAVES; w += 4) {
         uint64_t x[KMAX];
 #pragma unroll
-        for (int i = 0; i < KMAX; ++i) x[i] = sh.wl[w][h.col][i];
+        for (int i = 0; i < KMAX; ++i) x[i] = sh.wl[i][w][h.col];
         list_merge(r.list, x);
       }
       list_merge_pair<16>(r.list);
