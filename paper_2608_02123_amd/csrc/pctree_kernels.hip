@@ -1133,7 +1133,9 @@ __device__ void stream_block(const Plan& p, const Plan& sp, HeadShared<KMAX, kRo
 #pragma unroll
     for (int i = 0; i < RT; ++i) {
       const int t = t0 + wave + WAVES * i;
-      if (t < lds0) tile_step<DT, NCMAX, KMAX>(p, h, areg[i], bfrag, lreg[i], t, r);
+      int tt = t;
+      asm volatile("" : "+v"(tt));  // keep the key parts of a resident tile unhoisted
+      if (t < lds0) tile_step<DT, NCMAX, KMAX>(p, h, areg[i], bfrag, lreg[i], tt, r);
     }
 #pragma unroll
     for (int q = 0; q < LTW; ++q) {
@@ -1142,7 +1144,9 @@ __device__ void stream_block(const Plan& p, const Plan& sp, HeadShared<KMAX, kRo
         u32x4 a[NCMAX];
 #pragma unroll
         for (int c = 0; c < NCMAX; ++c) a[c] = wl[((size_t)j * NCMAX + c) * 64 + lane];
-        tile_step<DT, NCMAX, KMAX>(p, h, a, bfrag, llds[q], lds0 + j, r);
+        int tt = lds0 + j;
+        asm volatile("" : "+v"(tt));  // (as above)
+        tile_step<DT, NCMAX, KMAX>(p, h, a, bfrag, llds[q], tt, r);
       }
     }
     for (int t = str0 + wave; t < t1; t += WAVES) {
@@ -1217,9 +1221,14 @@ __device__ void stream_block_fold(const Plan& p, const Plan& sp,
       const int ta = t0 + wave + WAVES * (2 * q);
       const int tb = t0 + wave + WAVES * (2 * q + 1);
       const bool okb = 2 * q + 1 < RT && tb < lds0;
+      // the tile index is the same every stage; hidden from the compiler so
+      // that the token parts of its keys are recomputed (a few VALU ops)
+      // rather than hoisted out of the stage loop and spilled to scratch
+      int tt = h.half ? tb : ta;
+      asm volatile("" : "+v"(tt));
       if (ta < lds0)
-        tile_pair_step<DT, NCMAX, KMAX>(p, h, areg[2 * q], areg[i1], bfrag, lreg[q],
-                                        h.half ? tb : ta, h.half ? okb : true, r);
+        tile_pair_step<DT, NCMAX, KMAX>(p, h, areg[2 * q], areg[i1], bfrag, lreg[q], tt,
+                                        h.half ? okb : true, r);
     }
 #pragma unroll
     for (int q = 0; q < LP; ++q) {
@@ -1228,9 +1237,11 @@ __device__ void stream_block_fold(const Plan& p, const Plan& sp,
       if (ja < nlds) {
         const bool okb = 2 * q + 1 < LTW && jb < nlds;
         const int jl = okb ? jb : ja;
+        int tt = lds0 + (h.half ? jb : ja);
+        asm volatile("" : "+v"(tt));  // (as above)
         lds_pair_step<DT, NCMAX, KMAX>(p, h, wl + (size_t)ja * NCMAX * 64 + lane,
-                                       wl + (size_t)jl * NCMAX * 64 + lane, bfrag, llds[q],
-                                       lds0 + (h.half ? jb : ja), h.half ? okb : true, r);
+                                       wl + (size_t)jl * NCMAX * 64 + lane, bfrag, llds[q], tt,
+                                       h.half ? okb : true, r);
       }
     }
     for (int ta = str0 + wave; ta < t1; ta += 2 * WAVES) {
