@@ -454,7 +454,7 @@ __device__ __forceinline__ f32x4 mfma_chunk<0>(u32x4 a, u32x4 b, f32x4 acc) {
 // (token 0 stands in for an invalid root, whose tree is emitted empty), a
 // count of -1 that stays if the round is aborted, the trace's stage-0 row.
 // Threads [tid0, tid0 + nth) of the calling workgroup share the work.
-__device__ void init_request(const Plan& p, int req, int tid, int nth) {
+__device__ __forceinline__ void init_request_body(const Plan& p, int req, int tid, int nth) {
   int root = p.root[req];
   const bool bad = root < 0 || root >= p.V;
   if (bad) root = 0;
@@ -477,6 +477,10 @@ __device__ void init_request(const Plan& p, int req, int tid, int nth) {
       p.t_score[o] = first ? 0.0f : -INFINITY;
     }
   }
+}
+
+__device__ void init_request(const Plan& p, int req, int tid, int nth) {
+  init_request_body(p, req, tid, nth);
 }
 
 // Multi-launch form: request state in the workspace and the stage-0 head input.
@@ -1082,7 +1086,7 @@ __device__ __forceinline__ void init_front(const Plan& p, FrontShared& fs) {
 // fragment order, the rest re-read every stage), B stages of frontier
 // selection + head stream + partial publication.
 template <int DT, int NCMAX, int KMAX>
-__device__ void stream_block(const Plan& p, const Plan& sp, HeadShared<KMAX, kRoundWaves>& sh,
+__device__ __forceinline__ void stream_block(const Plan& p, const Plan& sp, HeadShared<KMAX, kRoundWaves>& sh,
                              FrontShared& fs, char* ul, u32x4* wl, int& sh_go) {
   constexpr int WAVES = kRoundWaves;
   constexpr int RT = resident_reg_tiles(NCMAX);
@@ -1310,8 +1314,9 @@ struct SelShared {
 // next frontier (the k' best of each request's layer, Sec. 4.1), merge them
 // into the running global top-N (Sec. 4.2) and write the next head input.
 // Needs blockDim >= 512 and nreq * P * k' <= 256.
-__device__ void stage_select(const Plan& p, const State& st, int d, int P, int req0, int nreq,
-                             SelShared& sh, bool act, bool bcast, bool shared = false) {
+__device__ __forceinline__ void stage_select_body(const Plan& p, const State& st, int d, int P,
+                                                  int req0, int nreq, SelShared& sh, bool act,
+                                                  bool bcast, bool shared) {
   const int tid = threadIdx.x;
   const int kk = p.kk;
   const int per_req = P * kk;
@@ -1408,6 +1413,15 @@ __device__ void stage_select(const Plan& p, const State& st, int d, int P, int r
   }
   __syncthreads();
   if (more && act) write_activations(p, st, d + 1, req0, nreq);
+}
+
+// The stage, init and emission routines have an out-of-line entry (used by the
+// multi-launch kernels and the k' <= 8 keepers) and an inlined body: a keeper
+// with k' = 16 that called them out of line kept a copy of its launch
+// arguments in scratch memory, so it inlines the bodies instead.
+__device__ void stage_select(const Plan& p, const State& st, int d, int P, int req0, int nreq,
+                             SelShared& sh, bool act, bool bcast, bool shared = false) {
+  stage_select_body(p, st, d, P, req0, nreq, sh, act, bcast, shared);
 }
 
 // The top-k' children and the lse of each of the R*P (<= 16) rows of stage d
@@ -1631,7 +1645,7 @@ __device__ void mask_rows(const int* par, int count, int N, uint32_t* out, uint3
 // every time).  The ancestor mask row of a node is its parent's row (done a
 // level earlier) plus its own bit.  Uses threads [0, 256) of the block
 // (N <= 256); all threads must call it.
-__device__ void emit_request(const Plan& p, const State& st, int req) {
+__device__ __forceinline__ void emit_request_body(const Plan& p, const State& st, int req) {
   constexpr int kBatch = 8;
   __shared__ int sh_node[kEmitThreads], sh_emit[kEmitThreads];
   __shared__ int sh_td[kEmitThreads];     // depth << 20 | token
@@ -1765,6 +1779,10 @@ __device__ void emit_request(const Plan& p, const State& st, int req) {
   __syncthreads();
 }
 
+__device__ void emit_request(const Plan& p, const State& st, int req) {
+  emit_request_body(p, st, req);
+}
+
 // LDS of the persistent round kernel shared by its stage code.
 __shared__ SelShared g_sel;
 __shared__ FrontShared g_front;
@@ -1827,7 +1845,13 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   uint64_t* s_top = (uint64_t*)(dyn + p.lds_top_offset);
   const State st{s_front_node, s_front_tok, s_front_score, s_top,
                  (int*)(s_top + (size_t)p.R * p.N)};
-  for (int req = 0; req < p.R; ++req) init_request(p, req, threadIdx.x, blockDim.x);
+  constexpr bool kInline = KMAX > 8;  // keeps the launch arguments out of scratch
+  for (int req = 0; req < p.R; ++req) {
+    if constexpr (kInline)
+      init_request_body(p, req, threadIdx.x, blockDim.x);
+    else
+      init_request(p, req, threadIdx.x, blockDim.x);
+  }
   for (int i = threadIdx.x; i < p.R * p.kk; i += blockDim.x) {
     const int r0 = p.root[i / p.kk];
     st.front_node[i] = 0;
@@ -1845,9 +1869,17 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   for (int d = 0; d < p.B; ++d) {
     const int P = d == 0 ? 1 : p.kk;
     if (!sel_merge<KMAX>(p, d, p.R * P, ssh)) return;
-    stage_select(p, st, d, P, 0, p.R, ssh, false, true);
+    if constexpr (kInline)
+      stage_select_body(p, st, d, P, 0, p.R, ssh, false, true, false);
+    else
+      stage_select(p, st, d, P, 0, p.R, ssh, false, true);
   }
-  for (int req = 0; req < p.R; ++req) emit_request(p, st, req);
+  for (int req = 0; req < p.R; ++req) {
+    if constexpr (kInline)
+      emit_request_body(p, st, req);
+    else
+      emit_request(p, st, req);
+  }
 }
 
 // ---------------------------------------------------------------------------
