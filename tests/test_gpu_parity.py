@@ -54,6 +54,29 @@ def test_workload_parity(name):
     say(f"[parity] {name}: {reps}")
 
 
+@pytest.mark.parametrize("k,N", [(16, 64), (1, 64), (8, 256)], ids=["k16", "k1", "N256"])
+def test_sweep_points_full_vocab(k, N):
+    """The Qwen3-4B large-block inputs (V = 151936, B = 16, r = 256) under the
+    other beam widths and budgets the benchmark sweeps: k = 16 (16 frontier
+    rows, the one keeper that inlines its stage code), the chain k = 1, and
+    the largest budget N = 256.  Every request in full against the oracle."""
+    w = CONFIGS["qwen4b_b16"]
+    say(f"[parity] qwen4b_b16 inputs with k={k} N={N}")
+    inp = _qwen4b_b16_inputs()
+    _, reps = check(inp, k, N)
+    say(f"[parity] qwen4b_b16 k={k} N={N}: {reps}")
+    assert w.V == 151936 and w.B == 16 and w.r == 256
+
+
+_CACHE = {}
+
+
+def _qwen4b_b16_inputs():
+    if "qwen4b_b16" not in _CACHE:
+        _CACHE["qwen4b_b16"] = make_inputs(CONFIGS["qwen4b_b16"])
+    return _CACHE["qwen4b_b16"]
+
+
 def test_batched_serving_parity():
     """Eight independent requests in one call (R = 8, k = 16, N = 128, r = 512)."""
     w = CONFIGS["qwen14b_b16_r8"]
