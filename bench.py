@@ -248,8 +248,8 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (the per-round "
-              "builder shards by request with no exchange; see DESIGN.md)", file=sys.stderr)
+        print("bench.py measures one GPU: no multi-GPU path is implemented (requests would "
+              "shard across GPUs with no exchange between them)", file=sys.stderr)
         sys.exit(2)
 
     import torch

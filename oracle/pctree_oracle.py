@@ -50,7 +50,7 @@ V^d paths, an exact best-first top-N search, the greedy chain of Eq. 1 for
 k = 1, the Shared-Markov control for a parent-independent head, the
 parent-independent scoring as the tree of a zero head, the W = 0 closed form, a hand-derived V = 4 example, and structural invariants.
 Parity unpinned by the paper: emission order, padding values and the
-activation rounding points above (this build's own specification).
+activation rounding points above (choices of this library, not of the paper).
 """
 from __future__ import annotations
 

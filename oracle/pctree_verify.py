@@ -42,7 +42,7 @@ exhaustive checking of every node's ancestor chain, the chain case (k = 1,
 where the rule is the plain longest matching prefix), row invariants and a
 hand-derived example in tests/golden/verify_hand.json.  Parity unpinned by
 the paper: the row order, the padding values and the malformed-input rules
-above (this build's own specification).
+above (choices of this library, not of the paper).
 """
 from __future__ import annotations
 
