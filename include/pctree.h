@@ -28,7 +28,14 @@
  *    enqueue work: they return before the GPU has run it, do no host<->device
  *    copies and never synchronise.  Results are valid once the stream reaches
  *    that point.  Calls are re-entrant; concurrent calls need distinct
- *    workspaces.
+ *    workspaces.  Exception: a round with at most 16 frontier rows (R * k'
+ *    <= 16) runs as ONE launch whose workgroups, one per compute unit,
+ *    exchange data while they run, so they must all be resident together.
+ *    Such rounds must not overlap another round (or other long kernels) on
+ *    the same device, e.g. on a second stream: a workgroup that cannot start
+ *    makes the others' bounded waits give up (after 2 s), and the round is
+ *    then abandoned (see pctree_tree.count).  Rounds on one stream are
+ *    always safe.
  *  - Argument checking happens on the host before anything is enqueued; on
  *    any error status no device work has been issued and nothing is written.
  *    No C++ exception crosses this interface.
@@ -112,14 +119,21 @@ typedef struct pctree_inputs {
  * ascending, then root-to-node token path lexicographically ascending, so
  * node 0 is the root (token x_t, parent -1, depth 0, logprob 0) and
  * parent[i] < i.  Rows i >= count[r] are padded with token = parent = depth =
- * position = -1 and logprob = -inf (mask rows: zero words). */
+ * position = -1 and logprob = -inf (mask rows: zero words).
+ *
+ * count[r] = -1 marks an abandoned round (see the single-launch exception
+ * under the conventions above): then every row of every request is padding
+ * and every mask word is zero; nothing of an earlier call's tree remains.
+ * The call itself has already returned PCTREE_OK, so a caller that may
+ * overlap rounds on one device checks count once the stream has run. */
 typedef struct pctree_tree {
   int32_t* token;    /* [R][N] draft token ids                                   */
   int32_t* parent;   /* [R][N] index of the parent node in the same row, -1 root */
   int32_t* depth;    /* [R][N] tree depth (root 0)                               */
   int32_t* position; /* [R][N] prefix_len + depth                                */
   float* logprob;    /* [R][N] joint path score s(c) (Eq. 4), root 0             */
-  int32_t* count;    /* [R]    min(N, pool size)                                 */
+  int32_t* count;    /* [R]    min(N, pool size); 0 for an invalid root; -1 if
+                        the round was abandoned (all rows padded)             */
   uint32_t* mask;    /* optional (may be NULL): [R][N][(N+31)/32] ancestor mask,
                         bit j%32 of word j/32 of row i is set iff node j is node
                         i or one of its ancestors (same layout as build_mask)    */
@@ -160,7 +174,8 @@ pctree_status pctree_build_mask(const int32_t* parent, const int32_t* count, int
  * mode of `shape` (topk and budget are ignored; modes PARENT and SHARED give
  * the same chain, INDEPENDENT the chain of argmax_v L_d).  chain_token [R][B+1] gets
  * x_t, y_0..y_{B-1}; chain_logprob [R][B+1] the cumulative log-probabilities
- * (0 for x_t).  Same workspace as pctree_build_tree. */
+ * (0 for x_t).  Same workspace as pctree_build_tree.  An abandoned round
+ * leaves every chain_token entry -1 and every chain_logprob -inf. */
 pctree_status pctree_chain_decode(const pctree_shape* shape, const pctree_inputs* in,
                                   int32_t* chain_token, float* chain_logprob, void* workspace,
                                   size_t workspace_bytes, void* stream);

@@ -1783,6 +1783,26 @@ __device__ void emit_request(const Plan& p, const State& st, int req) {
   emit_request_body(p, st, req);
 }
 
+// An abandoned round (a bounded wait ran out): every output row of every
+// request is written as padding, mask rows zero, and count = -1 marks the
+// abort, so that nothing of an earlier call's tree is left behind.  All
+// threads of the workgroup take part.
+__device__ __forceinline__ void abort_outputs(const Plan& p) {
+  const int n = p.R * p.N;
+  for (int e = threadIdx.x; e < n; e += blockDim.x) {
+    p.o_token[e] = -1;
+    p.o_parent[e] = -1;
+    p.o_depth[e] = -1;
+    p.o_position[e] = -1;
+    p.o_logprob[e] = -INFINITY;
+  }
+  if (p.o_mask) {
+    const size_t nw = (size_t)n * ((p.N + 31) / 32);
+    for (size_t e = threadIdx.x; e < nw; e += blockDim.x) p.o_mask[e] = 0u;
+  }
+  for (int req = threadIdx.x; req < p.R; req += blockDim.x) p.o_count[req] = -1;
+}
+
 // LDS of the persistent round kernel shared by its stage code.
 __shared__ SelShared g_sel;
 __shared__ FrontShared g_front;
@@ -1868,7 +1888,10 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   __syncthreads();
   for (int d = 0; d < p.B; ++d) {
     const int P = d == 0 ? 1 : p.kk;
-    if (!sel_merge<KMAX>(p, d, p.R * P, ssh)) return;
+    if (!sel_merge<KMAX>(p, d, p.R * P, ssh)) {
+      abort_outputs(p);
+      return;
+    }
     if constexpr (kInline)
       stage_select_body(p, st, d, P, 0, p.R, ssh, false, true, false);
     else
@@ -2346,8 +2369,14 @@ DeviceInfo device_info() {
 
 }  // namespace
 
+DebugConfig& debug_config() {
+  static DebugConfig cfg;
+  return cfg;
+}
+
 hipError_t launch_round(const Plan& p0, hipStream_t st) {
-  const bool narrow = p0.R * p0.kk <= kNarrowRows && p0.mode == 0;
+  const DebugConfig dbg = debug_config();
+  const bool narrow = p0.R * p0.kk <= kNarrowRows && p0.mode == 0 && !dbg.force_multilaunch;
   Plan p = p0;
   DeviceInfo di;
   RoundFn rfn = nullptr;
@@ -2358,7 +2387,8 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
     rfn = round_fn(p);
     // one streaming slice per remaining CU (at most kSlicesMax) plus the
     // selector block: every workgroup is resident at once
-    const int target = std::max(1, std::min(di.cus - 1, kRoundSlicesMax));
+    int target = std::max(1, std::min(di.cus - 1, kRoundSlicesMax));
+    if (dbg.round_slices > 0) target = std::min(target, dbg.round_slices);
     p.tiles_per_slice = (p.ntiles + target - 1) / target;
     p.G = (p.ntiles + p.tiles_per_slice - 1) / p.tiles_per_slice;
     // dynamic LDS: the frontier's head input, the keeper's top-N, then as
@@ -2394,7 +2424,9 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
   }
   p.tag = next_tag();
   if (narrow && fit > 0) {
-    p.spin_ticks = 2 * di.ticks_per_s;  // a stage never legitimately waits 2 s
+    // a stage never legitimately waits 2 s; tests may shorten the bound so
+    // that the waits give up (every workgroup still exits on its own)
+    p.spin_ticks = dbg.wait_ticks >= 0 ? dbg.wait_ticks : 2 * di.ticks_per_s;
     // no word of an earlier use of the workspace may carry the call's tag
     {
       const int n = p.stages * p.rows_max * p.G * (p.kmax + kRecWords) + p.stages * p.rows_max;

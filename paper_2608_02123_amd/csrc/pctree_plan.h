@@ -99,6 +99,15 @@ void plan_shape(Plan& p, int V, int B, int N, int k, int r, int R, int dtype);
 // Enqueue one full round on `stream`.
 hipError_t launch_round(const Plan& p, hipStream_t stream);
 
+// Process-wide diagnostic overrides of the launch (pctree_debug_set in
+// include/pctree_profile.h); the defaults leave every launch as planned.
+struct DebugConfig {
+  long long wait_ticks = -1;  // < 0: 2 s of device wall clock per bounded wait
+  int force_multilaunch = 0;  // nonzero: per-stage launches even for narrow rounds
+  int round_slices = 0;       // > 0: V-slices of the persistent round (else one per CU but one)
+};
+DebugConfig& debug_config();
+
 // Event bracketing of the dominant kernel (pctree_profile.hip): call
 // profile_mark() right before and right after each of its launches.
 bool profile_on();

@@ -1,5 +1,6 @@
-// Optional hipEvent bracketing of the dominant kernel's launches (see
-// include/pctree_profile.h).  Off by default; costs one branch per launch.
+// Optional hipEvent bracketing of the dominant kernel's launches, and the
+// diagnostic launch overrides (see include/pctree_profile.h).  Off by
+// default; costs one branch per launch.
 #include "pctree_profile.h"
 
 #include <mutex>
@@ -77,6 +78,18 @@ pctree_status pctree_profile_read(double* total_ms, int64_t* launches, const cha
   *launches = (int64_t)pairs;
   if (kernel) *kernel = r.kernel;
   r.used = 0;
+  return PCTREE_OK;
+}
+
+pctree_status pctree_debug_set(const pctree_debug_config* cfg) {
+  DebugConfig d;
+  if (cfg) {
+    if (cfg->round_slices < 0) return PCTREE_ERR_INVALID_ARGUMENT;
+    d.wait_ticks = cfg->wait_ticks < 0 ? -1 : (long long)cfg->wait_ticks;
+    d.force_multilaunch = cfg->force_multilaunch != 0;
+    d.round_slices = cfg->round_slices;
+  }
+  debug_config() = d;
   return PCTREE_OK;
 }
 

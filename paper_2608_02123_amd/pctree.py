@@ -13,6 +13,7 @@ import torch
 
 __all__ = [
     "PCTreeError",
+    "RoundAborted",
     "lib",
     "Shape",
     "workspace_bytes",
@@ -28,6 +29,8 @@ __all__ = [
     "TreeAttention",
     "TreeBuilder",
     "status_string",
+    "DebugConfig",
+    "debug_set",
     "F32",
     "BF16",
     "MODE_PARENT",
@@ -47,6 +50,15 @@ class PCTreeError(RuntimeError):
     def __init__(self, status: int, what: str):
         super().__init__(f"{what}: {status_string(status)}")
         self.status = status
+
+
+class RoundAborted(RuntimeError):
+    """A round was abandoned on the device (count = -1, every row padded)."""
+
+    def __init__(self, requests):
+        super().__init__(f"round abandoned for requests {list(requests)} (count = -1): a "
+                         "workgroup of the single-launch round did not start in time")
+        self.requests = list(requests)
 
 
 class Shape(ctypes.Structure):
@@ -72,6 +84,12 @@ class _Tree(ctypes.Structure):
 
 class _Trace(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("token", "parent_slot", "score")]
+
+
+class DebugConfig(ctypes.Structure):
+    """pctree_debug_config of include/pctree_profile.h (test-only launch overrides)."""
+    _fields_ = [("wait_ticks", ctypes.c_int64), ("force_multilaunch", ctypes.c_int32),
+                ("round_slices", ctypes.c_int32)]
 
 
 _lib = None
@@ -120,6 +138,8 @@ def lib() -> ctypes.CDLL:
                                           ctypes.POINTER(ctypes.c_int64),
                                           ctypes.POINTER(ctypes.c_char_p)]
         L.pctree_profile_read.restype = ctypes.c_int
+        L.pctree_debug_set.argtypes = [ctypes.POINTER(DebugConfig)]
+        L.pctree_debug_set.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -158,16 +178,49 @@ def workspace_bytes(V, B, N, k, r, R=1, dtype=BF16) -> int:
     return int(lib().pctree_workspace_bytes(ctypes.byref(make_shape(V, B, N, k, r, R, dtype))))
 
 
-def _inputs(L, E, Wt, h, root, prefix_len):
-    for name, t in (("L", L), ("E", E), ("Wt", Wt), ("h", h), ("root", root),
-                    ("prefix_len", prefix_len)):
-        if not t.is_cuda or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous device tensor")
-    if not (L.dtype == E.dtype == Wt.dtype):
-        raise TypeError("L, E and Wt must share one dtype")
-    if h.dtype != torch.float32 or root.dtype != torch.int32 or prefix_len.dtype != torch.int32:
-        raise TypeError("h must be float32; root and prefix_len int32")
+_TORCH_DTYPE = {F32: torch.float32, BF16: torch.bfloat16}
+
+
+def check_inputs(shape: Shape, L, E, Wt, h, root, prefix_len, *, device=True) -> None:
+    """Raise unless every input has exactly the layout ``shape`` describes:
+    ``L [R][B][V]``, ``E [V][r]`` and ``Wt [V][r]`` in the shape's dtype,
+    ``h [R][B][r]`` float32, ``root [R]`` and ``prefix_len [R]`` int32, all
+    contiguous (and on a GPU when ``device``).  The kernels index these
+    tensors by the shape alone, so a smaller tensor would be read past its end.
+    """
+    V, B, r, R = shape.vocab, shape.block, shape.rank, shape.requests
+    want = {
+        "L": (L, (R, B, V), _TORCH_DTYPE.get(shape.dtype)),
+        "E": (E, (V, r), _TORCH_DTYPE.get(shape.dtype)),
+        "Wt": (Wt, (V, r), _TORCH_DTYPE.get(shape.dtype)),
+        "h": (h, (R, B, r), torch.float32),
+        "root": (root, (R,), torch.int32),
+        "prefix_len": (prefix_len, (R,), torch.int32),
+    }
+    for name, (t, shp, dt) in want.items():
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{name} must be a torch tensor")
+        if dt is None or t.dtype != dt:
+            raise TypeError(f"{name} must be {dt}, got {t.dtype}")
+        if tuple(t.shape) != shp:
+            raise ValueError(f"{name} must have shape {shp}, got {tuple(t.shape)}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if device and not t.is_cuda:
+            raise ValueError(f"{name} must be a device tensor")
+
+
+def _inputs(shape, L, E, Wt, h, root, prefix_len):
+    check_inputs(shape, L, E, Wt, h, root, prefix_len)
     return _Inputs(*(t.data_ptr() for t in (L, E, Wt, h, root, prefix_len)))
+
+
+def check_counts(count) -> None:
+    """Raise RoundAborted if a request's count is -1 (waits for the stream)."""
+    c = count.cpu()
+    bad = (c == -1).nonzero().flatten().tolist()
+    if bad:
+        raise RoundAborted(bad)
 
 
 class TreeBuilder:
@@ -175,6 +228,8 @@ class TreeBuilder:
 
     ``run(L, E, Wt, h, root, prefix_len)`` enqueues one round on the current
     stream and returns the output tensors (overwritten by the next call).
+    With ``check=True`` it then waits for the round and raises
+    :class:`RoundAborted` if the device abandoned it (count = -1).
     """
 
     def __init__(self, V, B, N, k, r, R=1, dtype=BF16, device="cuda", mask=True, trace=False,
@@ -208,35 +263,46 @@ class TreeBuilder:
                                  self.out["trace_parent_slot"].data_ptr(),
                                  self.out["trace_score"].data_ptr())
 
-    def run(self, L, E, Wt, h, root, prefix_len, stream=None):
+    def run(self, L, E, Wt, h, root, prefix_len, stream=None, check=False):
         self.bind(L, E, Wt, h, root, prefix_len)
-        return self.launch(stream)
+        return self.launch(stream, check=check)
 
     def bind(self, L, E, Wt, h, root, prefix_len):
         """Check and remember the inputs once; ``launch()`` then only enqueues."""
-        self._inp = _inputs(L, E, Wt, h, root, prefix_len)
+        self._inp = _inputs(self.shape, L, E, Wt, h, root, prefix_len)
         self._keep = (L, E, Wt, h, root, prefix_len)
         self._args = (ctypes.byref(self.shape), ctypes.byref(self._inp), ctypes.byref(self._tree),
                       ctypes.byref(self._trace) if self._trace is not None else None,
                       ctypes.c_void_p(self.workspace.data_ptr()), self.workspace.numel())
 
-    def launch(self, stream=None):
+    def launch(self, stream=None, check=False):
         st = lib().pctree_build_tree(*self._args, _stream(stream))
         _check(st, "pctree_build_tree")
+        if check:
+            check_counts(self.out["count"])
         return self.out
 
 
 def build_tree(L, E, Wt, h, root, prefix_len, k, N, *, mask=True, trace=False, stream=None,
-               mode=MODE_PARENT):
+               mode=MODE_PARENT, check=True):
     """One round for tensors ``L [R][B][V]``, ``E [V][r]``, ``Wt [V][r]``, ``h [R][B][r]``.
 
     Returns a dict of freshly allocated output tensors (see include/pctree.h).
+    With ``check`` (the default) it waits for the round and raises
+    :class:`RoundAborted` if the device abandoned it.
     """
     R, B, V = L.shape
     r = E.shape[1]
     b = TreeBuilder(V, B, N, k, r, R, _dtype_code(L), device=L.device, mask=mask, trace=trace,
                     mode=mode)
-    return b.run(L, E, Wt, h, root, prefix_len, stream=stream)
+    return b.run(L, E, Wt, h, root, prefix_len, stream=stream, check=check)
+
+
+def debug_set(wait_ticks: int = -1, force_multilaunch: bool = False,
+              round_slices: int = 0) -> None:
+    """Test-only launch overrides (pctree_debug_set); no arguments restores the defaults."""
+    cfg = DebugConfig(int(wait_ticks), 1 if force_multilaunch else 0, int(round_slices))
+    _check(lib().pctree_debug_set(ctypes.byref(cfg)), "pctree_debug_set")
 
 
 def profile_enable(on: bool = True) -> None:
@@ -276,7 +342,7 @@ def chain_decode(L, E, Wt, h, root, prefix_len=None, stream=None, mode=MODE_PARE
     ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=L.device)
     toks = torch.empty(R, B + 1, dtype=torch.int32, device=L.device)
     lps = torch.empty(R, B + 1, dtype=torch.float32, device=L.device)
-    inp = _inputs(L, E, Wt, h, root, prefix_len)
+    inp = _inputs(shape, L, E, Wt, h, root, prefix_len)
     st = lib().pctree_chain_decode(ctypes.byref(shape), ctypes.byref(inp), _ptr(toks), _ptr(lps),
                                    ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream))
     _check(st, "pctree_chain_decode")

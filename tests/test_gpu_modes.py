@@ -65,14 +65,21 @@ def test_mode_workload_parity(mode, name):
     say(f"[modes] {mode} {name}: {reps}")
 
 
-def test_shared_batched_serving():
-    """Eight requests, k = 16, N = 128, r = 512; replay on a sample of requests."""
+_CACHE = {}
+
+
+@pytest.mark.parametrize("req", range(CONFIGS["qwen14b_b16_r8"].R))
+def test_shared_batched_serving(req):
+    """Eight requests, k = 16, N = 128, r = 512, Shared-Markov scoring: one
+    GPU call, every request replayed against the oracle."""
     w = CONFIGS["qwen14b_b16_r8"]
-    say(f"[modes] shared {w.name}")
-    inp = make_inputs(w)
-    out = run(inp, w.k, w.N, "shared")
-    reps = C.compare_batch(out, inp, w.k, w.N, requests=[0, 3, 7], mode="shared")
-    say(f"[modes] shared {w.name}: {reps}")
+    if "shared" not in _CACHE:
+        say(f"[modes] shared {w.name}")
+        inp = make_inputs(w)
+        _CACHE["shared"] = (inp, run(inp, w.k, w.N, "shared"))
+    inp, out = _CACHE["shared"]
+    reps = C.compare_batch(out, inp, w.k, w.N, requests=[req], mode="shared")
+    say(f"[modes] shared {w.name} request {req}: {reps}")
 
 
 def test_modes_differ_under_conditioning():

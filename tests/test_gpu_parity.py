@@ -47,11 +47,16 @@ def check(inp, k, N, requests=None, **kw):
 
 @pytest.mark.parametrize("name", ["tiny", "brute", "qwen4b_b7", "qwen8b_b7", "qwen4b_b16"])
 def test_workload_parity(name):
+    """The single-request workloads, bit-exact against the oracle: their
+    seeded inputs have no selection boundary closer than 1e-4 (the oracle's
+    own margins are >= 0.017), so the comparator must find every tree exact."""
     w = CONFIGS[name]
     say(f"[parity] {name}: V={w.V} B={w.B} N={w.N} k={w.k} r={w.r} R={w.R} {w.dtype}")
     inp = make_inputs(w)
     _, reps = check(inp, w.k, w.N)
     say(f"[parity] {name}: {reps}")
+    for rep in reps:
+        assert rep["exact"], f"{name}: near tie (min_gap {rep['min_gap']:.3g}), tree not exact"
 
 
 @pytest.mark.parametrize("k,N", [(16, 64), (1, 64), (8, 256)], ids=["k16", "k1", "N256"])
@@ -77,20 +82,38 @@ def _qwen4b_b16_inputs():
     return _CACHE["qwen4b_b16"]
 
 
-def test_batched_serving_parity():
-    """Eight independent requests in one call (R = 8, k = 16, N = 128, r = 512)."""
+def _serving_round():
+    """Inputs and the GPU output of the 8-request Qwen3-14B round (one call,
+    shared by the per-request comparisons below)."""
+    if "serving" not in _CACHE:
+        w = CONFIGS["qwen14b_b16_r8"]
+        say(f"[parity] {w.name}: V={w.V} B={w.B} N={w.N} k={w.k} r={w.r} R={w.R}")
+        inp = make_inputs(w)
+        _CACHE["serving"] = (inp, run_gpu(inp, w.k, w.N))
+    return _CACHE["serving"]
+
+
+# Requests of the seeded 8-request inputs with a selection boundary closer than
+# 1e-4 under the oracle's own float64 scores (request 0: two candidates
+# 4.8e-5 apart), where either choice is correct and the comparator checks
+# validity instead of bit-exactness.  Every other request has no boundary
+# closer than 6e-4 and must be bit-exact.
+SERVING_NEAR_TIES = {0}
+
+
+@pytest.mark.parametrize("req", range(CONFIGS["qwen14b_b16_r8"].R))
+def test_batched_serving_parity(req):
+    """Eight independent requests in one call (R = 8, k = 16, N = 128, r = 512):
+    each request's tree against the oracle's."""
     w = CONFIGS["qwen14b_b16_r8"]
-    say(f"[parity] {w.name}: V={w.V} B={w.B} N={w.N} k={w.k} r={w.r} R={w.R}")
-    inp = make_inputs(w)
-    out = run_gpu(inp, w.k, w.N)
-    kk = min(w.k, w.V)
-    pool = 1 + kk + (w.B - 1) * kk * kk
-    for req in range(w.R):  # exact structure of every request
-        g = C.gpu_to_numpy(out, req)
-        C.check_structure(g, int(inp["root"][req]), int(inp["prefix_len"][req]), w.N,
-                          min(w.N, pool))
-    reps = C.compare_batch(out, inp, w.k, w.N, requests=[0, 5])  # full replay on a sample
-    say(f"[parity] {w.name}: {reps}")
+    inp, out = _serving_round()
+    say(f"[parity] {w.name} request {req}")
+    reps = C.compare_batch(out, inp, w.k, w.N, requests=[req])
+    say(f"[parity] {w.name} request {req}: {reps}")
+    if req in SERVING_NEAR_TIES:
+        assert reps[0]["min_gap"] < C.TIE, "the recorded near tie is gone: make it exact"
+    else:
+        assert reps[0]["exact"], f"request {req}: near tie (min_gap {reps[0]['min_gap']:.3g})"
 
 
 SHAPES = [
