@@ -124,6 +124,50 @@ pctree_status enqueue(const Plan& p, void* stream) {
   return e == hipSuccess ? PCTREE_OK : PCTREE_ERR_HIP;
 }
 
+// The checks of pctree_build_tree that do not concern the workspace.
+pctree_status check_tree_args(const pctree_shape* shape, const pctree_inputs* in,
+                              const pctree_tree* out, const pctree_trace* trace) {
+  pctree_status st = check_shape(shape);
+  if (st != PCTREE_OK) return st;
+  if ((st = check_inputs(in)) != PCTREE_OK) return st;
+  if (!out || !out->token || !out->parent || !out->depth || !out->position || !out->logprob ||
+      !out->count)
+    return PCTREE_ERR_INVALID_ARGUMENT;
+  if (!aligned(out->token, 4) || !aligned(out->parent, 4) || !aligned(out->depth, 4) ||
+      !aligned(out->position, 4) || !aligned(out->logprob, 4) || !aligned(out->count, 4) ||
+      !aligned(out->mask, 4))
+    return PCTREE_ERR_INVALID_ARGUMENT;
+  if (trace && (!trace->token || !trace->parent_slot || !trace->score ||
+                !aligned(trace->token, 4) || !aligned(trace->parent_slot, 4) ||
+                !aligned(trace->score, 4)))
+    return PCTREE_ERR_INVALID_ARGUMENT;
+  return PCTREE_OK;
+}
+
+// Enqueue one round of a checked call on a workspace of at least
+// tree_bytes(shape) bytes at `ws` (256-byte aligned).
+pctree_status enqueue_tree(const pctree_shape* shape, const pctree_inputs* in,
+                           const pctree_tree* out, const pctree_trace* trace, char* ws,
+                           void* stream) {
+  Plan p{};
+  plan_shape(p, shape->vocab, shape->block, shape->budget, shape->topk, shape->rank,
+             shape->requests, shape->dtype);
+  carve_workspace(p, ws);
+  bind_inputs(p, in);
+  p.mode = shape->mode;
+  p.o_token = out->token;
+  p.o_parent = out->parent;
+  p.o_depth = out->depth;
+  p.o_position = out->position;
+  p.o_logprob = out->logprob;
+  p.o_count = out->count;
+  p.o_mask = out->mask;
+  p.t_token = trace ? trace->token : nullptr;
+  p.t_pslot = trace ? trace->parent_slot : nullptr;
+  p.t_score = trace ? trace->score : nullptr;
+  return enqueue(p, stream);
+}
+
 }  // namespace
 
 void plan_shape(Plan& p, int V, int B, int N, int k, int r, int R, int dtype) {
@@ -192,40 +236,11 @@ pctree_status pctree_build_tree(const pctree_shape* shape, const pctree_inputs* 
                                 const pctree_tree* out, const pctree_trace* trace,
                                 void* workspace, size_t workspace_bytes, void* stream) {
   try {
-    pctree_status st = check_shape(shape);
+    const pctree_status st = check_tree_args(shape, in, out, trace);
     if (st != PCTREE_OK) return st;
-    if ((st = check_inputs(in)) != PCTREE_OK) return st;
-    if (!out || !out->token || !out->parent || !out->depth || !out->position || !out->logprob ||
-        !out->count)
-      return PCTREE_ERR_INVALID_ARGUMENT;
-    if (!aligned(out->token, 4) || !aligned(out->parent, 4) || !aligned(out->depth, 4) ||
-        !aligned(out->position, 4) || !aligned(out->logprob, 4) || !aligned(out->count, 4) ||
-        !aligned(out->mask, 4))
-      return PCTREE_ERR_INVALID_ARGUMENT;
-    if (trace && (!trace->token || !trace->parent_slot || !trace->score ||
-                  !aligned(trace->token, 4) || !aligned(trace->parent_slot, 4) ||
-                  !aligned(trace->score, 4)))
-      return PCTREE_ERR_INVALID_ARGUMENT;
     if (!workspace || !aligned(workspace, 256)) return PCTREE_ERR_WORKSPACE;
-
-    Plan p{};
-    plan_shape(p, shape->vocab, shape->block, shape->budget, shape->topk, shape->rank,
-               shape->requests, shape->dtype);
-    if (workspace_bytes < carve_workspace(p, nullptr)) return PCTREE_ERR_WORKSPACE;
-    carve_workspace(p, (char*)workspace);
-    bind_inputs(p, in);
-    p.mode = shape->mode;
-    p.o_token = out->token;
-    p.o_parent = out->parent;
-    p.o_depth = out->depth;
-    p.o_position = out->position;
-    p.o_logprob = out->logprob;
-    p.o_count = out->count;
-    p.o_mask = out->mask;
-    p.t_token = trace ? trace->token : nullptr;
-    p.t_pslot = trace ? trace->parent_slot : nullptr;
-    p.t_score = trace ? trace->score : nullptr;
-    return enqueue(p, stream);
+    if (workspace_bytes < tree_bytes(shape)) return PCTREE_ERR_WORKSPACE;
+    return enqueue_tree(shape, in, out, trace, (char*)workspace, stream);
   } catch (...) {
     return PCTREE_ERR_HIP;
   }
