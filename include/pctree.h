@@ -161,6 +161,25 @@ pctree_status pctree_build_tree(const pctree_shape* shape, const pctree_inputs* 
                                 const pctree_tree* out, const pctree_trace* trace,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/* pctree_build_tree for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  The same round with the same kernels and results, but its
+ * workspace is a fixed array inside the library, PCTREE_NOALLOC_SCRATCH_BYTES
+ * bytes per device (each device the library runs on holds its copy until the
+ * process ends); the call allocates and frees nothing.  The caller still
+ * provides inputs and outputs.  Errors as for pctree_build_tree, plus
+ * PCTREE_ERR_WORKSPACE (before any device work) when the shape needs more
+ * than PCTREE_NOALLOC_SCRATCH_BYTES of workspace (pctree_workspace_bytes),
+ * and PCTREE_ERR_HIP if the array's device address cannot be looked up.
+ * Every call on one device shares that device's array: calls whose rounds
+ * can overlap on one device (other streams, other host threads) race and
+ * corrupt each other; calls ordered on one stream are safe.  Each call
+ * clears what it needs before use. */
+#define PCTREE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+pctree_status pctree_build_tree_noalloc(const pctree_shape* shape, const pctree_inputs* in,
+                                        const pctree_tree* out, const pctree_trace* trace,
+                                        void* stream);
+
 /* Ancestor-only tree attention mask from parent indices (App. A): row i of
  * request r admits node i and its ancestors.  parent [R][N], count [R] (as
  * emitted by pctree_build_tree), mask [R][N][(N+31)/32] uint32.  Rows at or

@@ -4,6 +4,7 @@
 #include "pctree.h"
 
 #include <algorithm>
+#include <mutex>
 
 #include "pctree_attention.h"
 #include "pctree_plan.h"
@@ -168,6 +169,39 @@ pctree_status enqueue_tree(const pctree_shape* shape, const pctree_inputs* in,
   return enqueue(p, stream);
 }
 
+// ---------------------------------------------------------------------------
+// Workspace of pctree_build_tree_noalloc: a fixed array in device memory, one
+// copy per device, held until the process ends.  In host code `scratch`
+// names a host-side stand-in, not device memory: its device address is
+// looked up once per device (with that device current) and only that
+// address is ever passed to a kernel.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = PCTREE_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+
+struct ScratchSlot {
+  std::once_flag once;
+  void* ptr = nullptr;
+  hipError_t err = hipErrorUnknown;
+};
+
+ScratchSlot g_scratch[kMaxDevices];
+
+// Device address of the current device's scratch array (nullptr on failure).
+void* scratch_address() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  ScratchSlot& s = g_scratch[dev];
+  std::call_once(s.once, [&s] {
+    void* ptr = nullptr;
+    s.err = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    s.ptr = s.err == hipSuccess ? ptr : nullptr;
+  });
+  return s.ptr;
+}
+
 }  // namespace
 
 void plan_shape(Plan& p, int V, int B, int N, int k, int r, int R, int dtype) {
@@ -241,6 +275,24 @@ pctree_status pctree_build_tree(const pctree_shape* shape, const pctree_inputs* 
     if (!workspace || !aligned(workspace, 256)) return PCTREE_ERR_WORKSPACE;
     if (workspace_bytes < tree_bytes(shape)) return PCTREE_ERR_WORKSPACE;
     return enqueue_tree(shape, in, out, trace, (char*)workspace, stream);
+  } catch (...) {
+    return PCTREE_ERR_HIP;
+  }
+}
+
+pctree_status pctree_build_tree_noalloc(const pctree_shape* shape, const pctree_inputs* in,
+                                        const pctree_tree* out, const pctree_trace* trace,
+                                        void* stream) {
+  try {
+    const pctree_status st = check_tree_args(shape, in, out, trace);
+    if (st != PCTREE_OK) return st;
+    // checked before any HIP call: a shape past the array's size is an error
+    if (tree_bytes(shape) > kScratchBytes) return PCTREE_ERR_WORKSPACE;
+    char* ws = (char*)scratch_address();
+    if (!ws) return PCTREE_ERR_HIP;
+    // the round clears every word it polls before use, so what an earlier
+    // call left in the array does not matter
+    return enqueue_tree(shape, in, out, trace, ws, stream);
   } catch (...) {
     return PCTREE_ERR_HIP;
   }

@@ -43,6 +43,7 @@ LIB_PATH = os.path.join(_HERE, "libpctree.so")
 
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 F32, BF16 = 0, 1
+NOALLOC_SCRATCH_BYTES = 32 << 20  # PCTREE_NOALLOC_SCRATCH_BYTES
 MODE_PARENT, MODE_SHARED, MODE_INDEPENDENT = 0, 1, 2  # pctree_mode
 
 
@@ -110,6 +111,9 @@ def lib() -> ctypes.CDLL:
         L.pctree_build_tree.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(_Inputs),
                                         ctypes.POINTER(_Tree), ctypes.POINTER(_Trace), vp, sz, vp]
         L.pctree_build_tree.restype = ctypes.c_int
+        L.pctree_build_tree_noalloc.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(_Inputs),
+                                                ctypes.POINTER(_Tree), ctypes.POINTER(_Trace), vp]
+        L.pctree_build_tree_noalloc.restype = ctypes.c_int
         L.pctree_build_mask.argtypes = [vp, vp, ctypes.c_int32, ctypes.c_int32, vp, vp]
         L.pctree_build_mask.restype = ctypes.c_int
         L.pctree_chain_decode.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(_Inputs), vp, vp,
@@ -233,13 +237,15 @@ class TreeBuilder:
     """
 
     def __init__(self, V, B, N, k, r, R=1, dtype=BF16, device="cuda", mask=True, trace=False,
-                 mode=MODE_PARENT):
+                 mode=MODE_PARENT, workspace=True):
         self.shape = make_shape(V, B, N, k, r, R, dtype, mode)
         nbytes = int(lib().pctree_workspace_bytes(ctypes.byref(self.shape)))
         if nbytes == 0:
             _check(lib().pctree_build_tree(ctypes.byref(self.shape), None, None, None, None, 0,
                                            None), "shape")
-        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        # workspace=False: only run_noalloc() (the library's own scratch array)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device) if workspace \
+            else None
         i32 = dict(dtype=torch.int32, device=device)
         self.out = {
             "token": torch.empty(R, N, **i32),
@@ -272,12 +278,24 @@ class TreeBuilder:
         self._inp = _inputs(self.shape, L, E, Wt, h, root, prefix_len)
         self._keep = (L, E, Wt, h, root, prefix_len)
         self._args = (ctypes.byref(self.shape), ctypes.byref(self._inp), ctypes.byref(self._tree),
-                      ctypes.byref(self._trace) if self._trace is not None else None,
-                      ctypes.c_void_p(self.workspace.data_ptr()), self.workspace.numel())
+                      ctypes.byref(self._trace) if self._trace is not None else None)
 
     def launch(self, stream=None, check=False):
-        st = lib().pctree_build_tree(*self._args, _stream(stream))
+        if self.workspace is None:
+            raise RuntimeError("this builder has no workspace: use run_noalloc()")
+        st = lib().pctree_build_tree(*self._args, ctypes.c_void_p(self.workspace.data_ptr()),
+                                     self.workspace.numel(), _stream(stream))
         _check(st, "pctree_build_tree")
+        if check:
+            check_counts(self.out["count"])
+        return self.out
+
+    def run_noalloc(self, L, E, Wt, h, root, prefix_len, stream=None, check=False):
+        """The same round through pctree_build_tree_noalloc: no workspace
+        argument, the library's fixed per-device scratch array instead."""
+        self.bind(L, E, Wt, h, root, prefix_len)
+        st = lib().pctree_build_tree_noalloc(*self._args, _stream(stream))
+        _check(st, "pctree_build_tree_noalloc")
         if check:
             check_counts(self.out["count"])
         return self.out
