@@ -32,16 +32,85 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(w):
+def algorithmic_bytes(w, w_once=False):
     """Bytes one round must move (W and L_d streamed once per depth; the
-    frontier's embedding rows and the depth features)."""
+    frontier's embedding rows and the depth features).  With ``w_once`` W
+    counts once per round: the floor for a kernel that keeps W on chip
+    across the B stages."""
     es = 2 if w.dtype == "bf16" else 4
     kk = min(w.k, w.V)
     sum_p = 1 + (w.B - 1) * kk  # frontier sizes b_0 = 1, b_d = k'
-    return (w.B * w.r * w.V * es            # W, once per depth, shared by all requests
+    return ((1 if w_once else w.B) * w.r * w.V * es  # W, shared by all requests
             + w.R * w.B * w.V * es          # L_d per request
             + w.R * sum_p * w.r * es        # E rows gathered for the frontier
             + w.R * w.B * w.r * 4)          # h_d
+
+
+def spread(xs):
+    """Median, 10th and 90th percentiles of a list of per-round times (us)."""
+    if not xs:
+        return None
+    s = sorted(xs)
+
+    def q(f):
+        return s[min(len(s) - 1, int(round(f * (len(s) - 1))))]
+    return {"median": q(0.5), "p10": q(0.1), "p90": q(0.9), "rounds": len(s)}
+
+
+def time_rounds(launch, steps, cold_steps, flush):
+    """Per-round durations (us) from events around each launch: ``steps``
+    back-to-back (warm) rounds, then ``cold_steps`` rounds each after a write
+    of ``flush`` (512 MiB, larger than the 256 MB Infinity Cache, as the
+    target model's forward would evict W), outside the events."""
+    import torch
+
+    def pairs(n, before=None):
+        ev = []
+        for _ in range(n):
+            if before is not None:
+                before()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            launch()
+            b.record()
+            ev.append((a, b))
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) * 1000.0 for a, b in ev]
+
+    warm = pairs(steps)
+    cold = pairs(cold_steps, before=lambda: flush.add_(1)) if cold_steps else []
+    return warm, cold
+
+
+def time_config(P, name, steps, cold_steps, flush):
+    """us/round (warm and cold) and the fraction of the HBM roofline of one
+    more workload, with the same timing as the headline."""
+    import torch
+    from paper_2608_02123_amd.synth import CONFIGS, make_inputs
+
+    w = CONFIGS[name]
+    log(f"[bench] workload {name}")
+    inp = make_inputs(w)
+    dev = P.device_inputs(inp)
+    b = P.TreeBuilder(w.V, w.B, w.N, w.k, w.r, w.R, P.BF16 if w.dtype == "bf16" else P.F32,
+                      mask=True)
+    b.bind(**dev)
+    for _ in range(5):
+        b.launch()
+    torch.cuda.synchronize()
+    warm, cold = time_rounds(b.launch, steps, cold_steps, flush)
+    out = b.launch(check=True)
+    nbytes = algorithmic_bytes(w)
+    ws, cs = spread(warm), spread(cold)
+    res = {"workload": f"V={w.V} B={w.B} N={w.N} k={w.k} r={w.r} R={w.R} {w.dtype}",
+           "warm_us": ws, "cold_us": cs, "algorithmic_bytes": nbytes,
+           "w_once_bytes": algorithmic_bytes(w, w_once=True),
+           "frac": nbytes / (ws["median"] * 1e-6) / 1e9 / HBM_PEAK_GBS,
+           "cold_frac": (nbytes / (cs["median"] * 1e-6) / 1e9 / HBM_PEAK_GBS) if cs else None,
+           "count": [int(c) for c in out["count"].cpu()]}
+    del b, dev, inp
+    torch.cuda.empty_cache()
+    return res
 
 
 def kernel_hash():
@@ -237,6 +306,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cold-steps", type=int, default=50)
+    ap.add_argument("--configs", default="tiny,qwen4b_b7,qwen8b_b7,qwen14b_b16_r8",
+                    help="other workloads timed in the same run (comma list; empty: none)")
+    ap.add_argument("--config-steps", type=int, default=100)
     ap.add_argument("--no-verify", action="store_true",
                     help="skip timing the verification steps after the round")
     ap.add_argument("--sweep", action="store_true",
@@ -304,24 +376,19 @@ def main():
     per_launch = bytes_round if kname == "round_kernel" else bytes_round / w.B
     achieved = per_launch / k_avg_s / 1e9
 
-    # cold-MALL rounds: a 512 MiB write between rounds evicts W from the
-    # 256 MB Infinity Cache, as the target model's forward would
-    log(f"[bench] cold-cache pass {args.cold_steps}")
+    # per-round spread, warm (back to back) and cold (W evicted from the
+    # Infinity Cache before each round)
+    log(f"[bench] per-round pass: {args.steps} warm, {args.cold_steps} cold")
     flush = torch.empty(512 << 20 if args.cold_steps else 1, dtype=torch.uint8, device="cuda")
-    cold = []
-    for _ in range(args.cold_steps):
-        flush.add_(1)
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        builder.launch()
-        b.record()
-        cold.append((a, b))
-    torch.cuda.synchronize()
-    cold_ms = sorted(x.elapsed_time(y) for x, y in cold)
-    cold_med = cold_ms[len(cold_ms) // 2] if cold_ms else None
+    warm_us, cold_us = time_rounds(builder.launch, args.steps, args.cold_steps, flush)
+    warm_sp, cold_sp = spread(warm_us), spread(cold_us)
+    cold_med = cold_sp["median"] / 1000.0 if cold_sp else None  # ms
 
     verify = None if args.no_verify else time_verify(P, builder, w, inp)
     sweep = time_sweeps(P, w, inp, dev) if args.sweep else None
+    configs = {}
+    for name in [c for c in args.configs.split(",") if c and c != w.name]:
+        configs[name] = time_config(P, name, args.config_steps, min(args.cold_steps, 30), flush)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -329,6 +396,7 @@ def main():
         cpu = cpu_baseline(inp, w, args.cpu_seconds)
 
     traffic = measured_traffic()
+    w_once = algorithmic_bytes(w, w_once=True)
     line = {
         "metric": METRIC,
         "value": rounds_per_s,
@@ -347,14 +415,30 @@ def main():
                    "parallelism": "single GPU"},
         "us_per_round": ms * 1000.0,
         "round_hbm_frac": bytes_round / (ms / 1000.0) / 1e9 / HBM_PEAK_GBS,
+        "round_us": {"warm": warm_sp, "cold": cold_sp},
         "cold_us_per_round": cold_med * 1000.0 if cold_med else None,
+        "cold_rounds_per_s": 1000.0 / cold_med if cold_med else None,
         "cold_round_hbm_frac": (bytes_round / (cold_med / 1000.0) / 1e9 / HBM_PEAK_GBS
                                 if cold_med else None),
         "algorithmic_bytes_per_round": bytes_round,
+        "w_once_bytes_per_round": w_once,
         "roofline": {"bound": "hbm", "kernel": kname, "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic, "bytes_per_launch": per_launch,
-                     "avg_launch_us": k_avg_s * 1e6, "launches": launches},
+                     "avg_launch_us": k_avg_s * 1e6, "launches": launches,
+                     # the same bytes over the median cold round (W evicted first)
+                     "cold_frac": (bytes_round / (cold_med / 1000.0) / 1e9 / HBM_PEAK_GBS
+                                   if cold_med else None),
+                     # what the kernel really moves: counter bytes per launch
+                     "traffic_frac": (traffic / k_avg_s / 1e9 / HBM_PEAK_GBS
+                                      if traffic else None),
+                     # the floor with W read once per round, over the same time
+                     "w_once_bytes": w_once if kname == "round_kernel" else w_once / w.B,
+                     "w_once_frac": ((w_once if kname == "round_kernel" else w_once / w.B)
+                                     / k_avg_s / 1e9 / HBM_PEAK_GBS),
+                     # the B dependent stages of one launch: time per stage
+                     "stage_period_us": (k_avg_s * 1e6 / w.B if kname == "round_kernel"
+                                         else k_avg_s * 1e6)},
         "cpu_baseline": cpu,
         "wall_s_timed_region": wall,
     }
@@ -362,6 +446,8 @@ def main():
         line["verify"] = verify
     if sweep is not None:
         line["sweep"] = sweep
+    if configs:
+        line["configs"] = configs
     print(json.dumps(line), flush=True)
 
 

@@ -35,3 +35,15 @@ def test_more_than_one_gpu_exits_with_a_message():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+def test_w_once_bytes_qwen4b_b16():
+    # W counted once per round (the on-chip floor), the rest as above:
+    # 256 * 151936 * 2 = 77,791,232, + 4,861,952 + 61,952 + 16,384 = 82,731,520
+    assert bench.algorithmic_bytes(CONFIGS["qwen4b_b16"], w_once=True) == 82_731_520
+
+
+def test_spread_percentiles():
+    sp = bench.spread([float(x) for x in range(1, 12)])  # 1 .. 11
+    assert sp == {"median": 6.0, "p10": 2.0, "p90": 10.0, "rounds": 11}
+    assert bench.spread([]) is None
