@@ -49,6 +49,10 @@ typedef struct pctree_debug_config {
   int32_t round_slices;      /* > 0: at most this many vocabulary slices in the
                                 single-launch round (default 0: one per compute
                                 unit but one, at most 256)                       */
+  int32_t wide_unbounded;    /* nonzero: stages with more than 16 frontier rows
+                                ignore each row's lower bound of its k'-th best
+                                logit, so every logit is a candidate and every
+                                (row, slice) takes the exact per-slice path      */
 } pctree_debug_config;
 
 /* Install `cfg` (NULL restores the defaults).  PCTREE_ERR_INVALID_ARGUMENT if

@@ -250,8 +250,12 @@ size_t carve_workspace(Plan& p, char* base) {
   p.part_hd = (uint64_t*)take(parts * kRecWords * sizeof(uint64_t));
   p.req_bad = (int*)take(R * sizeof(int));
   p.front_w = (uint64_t*)take((size_t)p.stages * p.rows_max * sizeof(uint64_t));
-  p.mrow_key = (uint64_t*)take((size_t)p.rows_max * p.kmax * sizeof(uint64_t));
-  p.mrow_lse = (float*)take((size_t)p.rows_max * sizeof(float));
+  p.tau = (float*)take((size_t)p.rows_max * sizeof(float));
+  p.probe_tok = (int*)take(R * (size_t)p.B * kProbe * sizeof(int));
+  p.probe_w = take(R * (size_t)p.B * kProbe * p.r * es);
+  p.probe_l = (float*)take(R * (size_t)p.B * kProbe * sizeof(float));
+  p.thr_ms = (float*)take((size_t)p.rows_max * kSlicesMax * 2 * sizeof(float));
+  p.thr_cnt = (int*)take((size_t)p.rows_max * kSlicesMax * sizeof(int));
   return off;
 }
 

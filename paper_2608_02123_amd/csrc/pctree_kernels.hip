@@ -27,6 +27,7 @@
 //   node key  = ord(score) << 32 | (63-depth) << 26 | (2^20-1-token) << 6 | (63-slot)
 //                                         (score desc, depth asc, token asc, slot asc)
 // where ord() maps a float onto an unsigned integer of the same order (-0 -> +0).
+#include "pctree.h"
 #include "pctree_plan.h"
 
 #include <math.h>
@@ -145,84 +146,24 @@ __device__ __forceinline__ float load_elem(const void* base, size_t i) {
   return ((const float*)base)[i];
 }
 
-// One head-input element of row `row` (request-major rows of kk slots):
-// u = act(E[tok][j], h[req][d][j]) stored at the head's precision.
-__device__ __forceinline__ void put_activation(const Plan& p, size_t row, int tok, int j,
-                                               float hj) {
-  const size_t o = row * p.r + j;
-  if (p.dtype) {
-    const float ej =
-        __uint_as_float((uint32_t)((const uint16_t*)p.E)[(size_t)tok * p.r + j] << 16);
-    ((uint16_t*)p.U)[o] = silu_bf16(ej, hj);
-  } else {
-    ((float*)p.U)[o] = silu_f32(((const float*)p.E)[(size_t)tok * p.r + j], hj);
-  }
-}
-
-// A zero head input: the parent-independent mode scores every parent with the
-// base logits alone, z = L_d + 0 (the projection of a zero row is exactly 0).
-__device__ __forceinline__ void put_zero_activation(const Plan& p, size_t row, int j) {
-  const size_t o = row * p.r + j;
-  if (p.dtype)
-    ((uint16_t*)p.U)[o] = 0;
-  else
-    ((float*)p.U)[o] = 0.0f;
-}
-
 // Selection state of a round: the frontier (slot-indexed, kk per request) and
 // the running global top-N (sorted keys and pool ids, N per request).  It
 // lives in the workspace for the multi-launch form and in the selector
 // workgroup's LDS for the persistent form.
+// Entry i of request req sits at [(req - rbase) * kk + slot] (frontier) and
+// [(req - rbase) * N + i] (top-N): rbase 0 for state holding every request,
+// req for a copy of one request's.
 struct State {
   int* front_node;
   int* front_tok;
   float* front_score;
   uint64_t* top_key;
   int* top_node;
+  int rbase;
 };
 
 __device__ __forceinline__ State global_state(const Plan& p) {
-  return State{p.front_node, p.front_tok, p.front_score, p.top_key, p.top_node};
-}
-
-// Head inputs of the frontier used at stage `d` for requests [req0, req0+nreq).
-// Each thread issues the loads of four elements before computing any of them.
-__device__ void write_activations(const Plan& p, const State& st, int d, int req0, int nreq) {
-  constexpr int kBatch = 4;
-  const int per_req = p.kk * p.r;
-  const int n = nreq * per_req;
-  for (int base = 0; base < n; base += kBatch * blockDim.x) {
-    size_t erow[kBatch], urow[kBatch], hrow[kBatch];
-    uint32_t ev[kBatch];
-    float hv[kBatch];
-#pragma unroll
-    for (int q = 0; q < kBatch; ++q) {
-      const int e = min(base + q * (int)blockDim.x + (int)threadIdx.x, n - 1);
-      const int rq = e / per_req;
-      const int rem = e - rq * per_req;
-      const int slot = rem / p.r;
-      const int j = rem - slot * p.r;
-      const int req = req0 + rq;
-      erow[q] = (size_t)min(max(st.front_tok[req * p.kk + slot], 0), p.V - 1) * p.r + j;
-      urow[q] = ((size_t)req * p.kk + slot) * p.r + j;
-      hrow[q] = ((size_t)req * p.B + d) * p.r + j;
-    }
-#pragma unroll
-    for (int q = 0; q < kBatch; ++q) {
-      ev[q] = p.dtype ? (uint32_t)((const uint16_t*)p.E)[erow[q]] << 16
-                      : ((const uint32_t*)p.E)[erow[q]];
-      hv[q] = p.h[hrow[q]];
-    }
-#pragma unroll
-    for (int q = 0; q < kBatch; ++q) {
-      if (base + q * (int)blockDim.x + (int)threadIdx.x < n) {
-        if (p.dtype)
-          ((uint16_t*)p.U)[urow[q]] = silu_bf16(__uint_as_float(ev[q]), hv[q]);
-        else
-          ((float*)p.U)[urow[q]] = silu_f32(__uint_as_float(ev[q]), hv[q]);
-      }
-    }
-  }
+  return State{p.front_node, p.front_tok, p.front_score, p.top_key, p.top_node, 0};
 }
 
 // ---------------------------------------------------------------------------
@@ -483,26 +424,12 @@ __device__ void init_request(const Plan& p, int req, int tid, int nth) {
   init_request_body(p, req, tid, nth);
 }
 
-// Multi-launch form: request state in the workspace and the stage-0 head input.
-__global__ __launch_bounds__(kEmitThreads) void prologue_kernel(Plan p) {
-  const int req = blockIdx.x;
-  const int tid = threadIdx.x;
-  init_request(p, req, tid, blockDim.x);
-  int root = p.root[req];
-  if (root < 0 || root >= p.V) root = 0;
-  if (tid == 0) {
-    p.top_key[(size_t)req * p.N] = node_key(0.0f, 0, root, 0);
-    p.top_node[(size_t)req * p.N] = 0;
-    p.front_node[req * p.kk] = 0;
-    p.front_tok[req * p.kk] = root;
-    p.front_score[req * p.kk] = 0.0f;
-  }
-  for (int j = tid; j < p.r; j += blockDim.x) {
-    if (p.mode == 2)
-      put_zero_activation(p, (size_t)req * p.kk, j);
-    else
-      put_activation(p, (size_t)req * p.kk, root, j, p.h[(size_t)req * p.B * p.r + j]);
-  }
+// Head rows per request of stage d, and whether stage d runs the wide form.
+__device__ __host__ __forceinline__ int head_rows(int mode, int d, int kk) {
+  return (d == 0 || mode != 0) ? 1 : kk;
+}
+__device__ __host__ __forceinline__ bool stage_wide(int mode, int d, int R, int kk) {
+  return R * head_rows(mode, d, kk) > kNarrowRows;
 }
 
 // ---------------------------------------------------------------------------
@@ -1300,6 +1227,7 @@ __device__ __forceinline__ int count_greater(const uint64_t* keys, int n, uint64
 }
 
 struct SelShared {
+  int next_tok[kNarrowRows];  // tokens of the next frontier, by slot (request-major)
   uint64_t rowkeys[kNarrowRows][16];  // top-k' children (child keys) of each row
   float lse[kNarrowRows];
   __attribute__((aligned(16))) uint64_t ckey[256];  // node keys of the stage's candidates
@@ -1315,7 +1243,7 @@ struct SelShared {
 // into the running global top-N (Sec. 4.2) and write the next head input.
 // Needs blockDim >= 512 and nreq * P * k' <= 256.
 __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st, int d, int P,
-                                                  int req0, int nreq, SelShared& sh, bool act,
+                                                  int req0, int nreq, SelShared& sh,
                                                   bool bcast, bool shared) {
   const int tid = threadIdx.x;
   const int kk = p.kk;
@@ -1338,8 +1266,8 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
     // corrupted key from indexing out of bounds
     tok = min(max(child_key_token(ck), 0), p.V - 1);
     const float lp = child_key_value(ck) - sh.lse[lrow];
-    score = st.front_score[req * kk + pr] + lp;
-    par = st.front_node[req * kk + pr];
+    score = st.front_score[(req - st.rbase) * kk + pr] + lp;
+    par = st.front_node[(req - st.rbase) * kk + pr];
     sh.ckey[tid] = node_key(score, d + 1, tok, pr);
   }
   // (the frontier's loads above have returned: LDS barriers suffice until
@@ -1362,9 +1290,10 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
                          ((uint64_t)__float_as_uint(score) << 32) |
                              ((uint64_t)tok << kTagBits) | p.tag,
                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    st.front_node[req * kk + slot] = nbase + ci;
-    st.front_tok[req * kk + slot] = tok;
-    st.front_score[req * kk + slot] = score;
+    st.front_node[(req - st.rbase) * kk + slot] = nbase + ci;
+    st.front_tok[(req - st.rbase) * kk + slot] = tok;
+    st.front_score[(req - st.rbase) * kk + slot] = score;
+    if (rq * kk + slot < kNarrowRows) sh.next_tok[rq * kk + slot] = tok;
     if (p.t_token) {
       const size_t o = ((size_t)req * p.B + d + 1) * p.k + slot;
       p.t_token[o] = tok;
@@ -1383,15 +1312,17 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
   }
   // running global top-N, one request at a time: every element's new
   // position is its rank in the union (both sides are sorted), computed
-  // before any element moves
+  // before any element moves.  The state is in LDS (every caller keeps a
+  // copy there), so LDS barriers order it; the global stores above need no
+  // wait until the barrier that ends the stage.
   const int ncur = min(p.N, nbase);
   for (int rq = 0; rq < nreq; ++rq) {
     const int req = req0 + rq;
-    uint64_t* tk = st.top_key + (size_t)req * p.N;
-    int* tn = st.top_node + (size_t)req * p.N;
-    __syncthreads();
+    uint64_t* tk = st.top_key + (size_t)(req - st.rbase) * p.N;
+    int* tn = st.top_node + (size_t)(req - st.rbase) * p.N;
+    lds_barrier();
     for (int i = tid; i < ncur; i += blockDim.x) sh.tkey[i] = tk[i];
-    __syncthreads();
+    lds_barrier();
     int pos = p.N, node = 0;
     uint64_t key = 0;
     if (tid < per_req) {
@@ -1405,14 +1336,13 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
       pos = i + count_greater(sh.ckey + rq * per_req, per_req, key);
       node = tn[i];
     }
-    __syncthreads();
+    lds_barrier();
     if (pos < p.N) {
       tk[pos] = key;
       tn[pos] = node;
     }
   }
   __syncthreads();
-  if (more && act) write_activations(p, st, d + 1, req0, nreq);
 }
 
 // The stage, init and emission routines have an out-of-line entry (used by the
@@ -1420,8 +1350,8 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
 // with k' = 16 that called them out of line kept a copy of its launch
 // arguments in scratch memory, so it inlines the bodies instead.
 __device__ void stage_select(const Plan& p, const State& st, int d, int P, int req0, int nreq,
-                             SelShared& sh, bool act, bool bcast, bool shared = false) {
-  stage_select_body(p, st, d, P, req0, nreq, sh, act, bcast, shared);
+                             SelShared& sh, bool bcast, bool shared = false) {
+  stage_select_body(p, st, d, P, req0, nreq, sh, bcast, shared);
 }
 
 // The top-k' children and the lse of each of the R*P (<= 16) rows of stage d
@@ -1668,7 +1598,7 @@ __device__ __forceinline__ void emit_request_body(const Plan& p, const State& st
   float score = 0.0f;
   if (tid < count0) {
     // (clamped: an inconsistent state must not address outside the pool)
-    node = min(max(st.top_node[(size_t)req * p.N + tid], 0), p.maxpool - 1);
+    node = min(max(st.top_node[(size_t)(req - st.rbase) * p.N + tid], 0), p.maxpool - 1);
     dep = p.node_depth[pb + node];
     tok = p.node_tok[pb + node];
     pnode = p.node_par[pb + node];
@@ -1864,7 +1794,7 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   __shared__ float s_front_score[kNarrowRows];
   uint64_t* s_top = (uint64_t*)(dyn + p.lds_top_offset);
   const State st{s_front_node, s_front_tok, s_front_score, s_top,
-                 (int*)(s_top + (size_t)p.R * p.N)};
+                 (int*)(s_top + (size_t)p.R * p.N), 0};
   constexpr bool kInline = KMAX > 8;  // keeps the launch arguments out of scratch
   for (int req = 0; req < p.R; ++req) {
     if constexpr (kInline)
@@ -1893,9 +1823,9 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
       return;
     }
     if constexpr (kInline)
-      stage_select_body(p, st, d, P, 0, p.R, ssh, false, true, false);
+      stage_select_body(p, st, d, P, 0, p.R, ssh, true, false);
     else
-      stage_select(p, st, d, P, 0, p.R, ssh, false, true);
+      stage_select(p, st, d, P, 0, p.R, ssh, true);
   }
   for (int req = 0; req < p.R; ++req) {
     if constexpr (kInline)
@@ -1923,207 +1853,337 @@ __global__ __launch_bounds__(kHeadThreads) void head_kernel(Plan p, int d, int P
   head_slice<DT, NCMAX, KMAX, kHeadThreads / 64>(p, d, P, cb, slice, hsh);
 }
 
-// After the rows of stage d are in sh (top-k' children, lse): the stage
-// selection of request req, and for the two control modes the next stage's
-// single head input.
-__device__ void select_tail(const Plan& p, int d, int P, int req, SelShared& ssh) {
-  if (p.mode == 0) {
-    stage_select(p, global_state(p), d, P, req, 1, ssh, true, false);
-    return;
-  }
-  // Shared-Markov and parent-independent modes: the one row of the stage
-  // (P = 1) serves every frontier parent of the tree
-  stage_select(p, global_state(p), d, d == 0 ? 1 : p.kk, req, 1, ssh, false, false, true);
-  if (d + 1 < p.B) {
-    // next head input: the greedy chain's token (Shared-Markov), or zero
-    const int tok = min(max(child_key_token(ssh.rowkeys[0][0]), 0), p.V - 1);
-    const float* hrow = p.h + ((size_t)req * p.B + d + 1) * p.r;
-    for (int j = threadIdx.x; j < p.r; j += blockDim.x) {
-      if (p.mode == 2)
-        put_zero_activation(p, (size_t)req * p.kk, j);
-      else
-        put_activation(p, (size_t)req * p.kk, tok, j, hrow[j]);
-    }
-  }
-}
-
 // ---------------------------------------------------------------------------
-// multi-launch form, wide frontiers (more than 16 rows per stage)
+// wide stages (more than 16 frontier rows): per-row bounds from probe tokens
 // ---------------------------------------------------------------------------
-constexpr int kWideWaves = 8;      // column blocks of 16 rows one workgroup serves
-constexpr int kWideAhead = 3;      // W tiles in flight per workgroup beyond the one in LDS
-constexpr int kMergeThreads = 256;
+// A row's k' children are its k' best logits.  Any k' logits of the row are
+// at most as large as the k'-th best, so the k'-th best of the row's logits
+// at a few probe tokens is a lower bound tau of it: a token whose logit lies
+// below tau cannot be a child.  The probe tokens of a (request, depth) are
+// about the kProbe largest base logits L_d (found once per round); the head
+// stream of a wide stage then keeps, per row, the online (max, sum of exp)
+// of every logit but only the rare logits at or above tau.  The bound is
+// lowered by a margin that covers the difference between the probe's
+// float32 dot products and the MFMA's (both sum r bf16 products in float32,
+// in different orders).
 
-// Publish one wave's rows (column block) of a slice: the four lanes of a row
-// merge their lists and (max, sum) pairs, and the first writes the slice
-// record and list of stage 0's buffers (read by the next launch).
-template <int KMAX>
-__device__ __forceinline__ void publish_wave(const Plan& p, const HeadLane& h, int slice,
-                                             RowAcc<KMAX>& r) {
-  float m = r.m, sum = r.s;
-  list_merge_pair<16>(r.list);
-  lse_combine_pair<16>(m, sum);
-  list_merge_pair<32>(r.list);
-  lse_combine_pair<32>(m, sum);
-  if (h.grp == 0 && h.row_ok) {
-    uint64_t* hd = slice_record(p, 0, h.row) + slice;
-#pragma unroll
-    for (int i = 0; i < kHeadKeys; ++i)
-      __hip_atomic_store(hd + i * kSlicesMax, (i < KMAX ? r.list[i < KMAX ? i : 0] : 0ull) | p.tag,
-                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(hd + kHeadKeys * kSlicesMax, ((uint64_t)p.tag << 32) | __float_as_uint(sum),
-                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    uint64_t* dst = p.part_key + ((size_t)h.row * kSlicesMax + slice) * KMAX;
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i)
-      __hip_atomic_store(dst + i, r.list[i] | p.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
+// Probe tokens of every (request, depth): each thread keeps the largest base
+// logit among the tokens it scans (ties: lowest id), each wave the kProbeWave
+// best of its threads', and the kProbe best of those become the probes
+// (fewer when V < kProbe).  Any tokens would give a valid bound; these make
+// it tight.
+constexpr int kProbeThreads = 1024;
+constexpr int kProbeWave = 4;
+
+__device__ __forceinline__ uint64_t probe_key(float z, int v) {
+  return ((uint64_t)f32_ord(z) << 32) | (uint32_t)(0x7FFFFFFF - v);
 }
 
-// One V-slice for up to kWideWaves column blocks of 16 frontier rows (wave w
-// holds block 8 * group + w, its rows' head input in registers for the whole
-// slice).  Each W tile is read from memory once per workgroup: all waves
-// fetch a share of its rank chunks and store them in LDS in MFMA fragment
-// order, then every wave multiplies the whole tile with its own rows.  Two
-// LDS buffers: tile t + 1 is fetched while tile t is multiplied.  The grid
-// has 8 * ceil(G / 8) * (column groups) workgroups, in the XCD-aware order
-// of head_kernel.
-template <int DT, int NCMAX, int KMAX>
-__global__ __launch_bounds__(kWideWaves * 64) void head_wide_kernel(Plan p, int d, int P) {
-  constexpr int KC = DT ? 32 : 16;  // rank elements per 16x16 MFMA step
-  constexpr int ESZ = DT ? 2 : 4;
-  constexpr int CPW = (NCMAX + kWideWaves - 1) / kWideWaves;  // chunks one wave fetches
-  __shared__ u32x4 tiles[2][NCMAX][64];
-  const int ncb = (p.R * P + kTile - 1) / kTile;
-  const int ngrp = (ncb + kWideWaves - 1) / kWideWaves;
-  const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
-  const int grp = j % ngrp;
-  const int slice = (j / ngrp) * 8 + x;
-  if (slice >= p.G) return;  // the whole workgroup
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int cb = grp * kWideWaves + wave;
-  const bool live = cb < ncb;  // waves past the last block only fetch
-  const HeadLane h(p, P, live ? cb : 0);
-  u32x4 bfrag[NCMAX];
-  if (live) load_bfrag<DT, NCMAX>(p, h, bfrag);
-  RowAcc<KMAX> r;
-  r.init();
-  const int t0 = slice * p.tiles_per_slice;
-  const int t1 = min(t0 + p.tiles_per_slice, p.ntiles);
-  // lane l fetches what lane l of a consumer feeds the MFMA: token l % 16 of
-  // the tile (clamped into the vocabulary), rank group l / 16; chunks past
-  // the rank re-read the last one (finite values that meet zero B fragments)
-  auto fetch = [&](int t, u32x4 (&dst)[CPW]) {
-    const int tok = min(t * kTile + (lane & 15), p.V - 1);
-    const char* wrow = (const char*)p.Wt + ((size_t)tok * p.r + (lane >> 4) * (KC / 4)) * ESZ;
+template <int DT>
+__device__ __forceinline__ uint64_t probe_scan(const Plan& p, size_t base) {
+  constexpr int ES = DT ? 2 : 4;
+  constexpr int PER = 16 / ES;  // elements per 16-byte load
+  const int tid = threadIdx.x;
+  uint64_t k = 0;
+  // elements before the first 16-byte boundary of the row, and after the last
+  const int head = (int)(((16 - (base * ES) % 16) % 16) / ES);
+  const int nvec = (p.V - min(head, p.V)) / PER;
+  const int tail0 = head + nvec * PER;
+  if (tid < head && tid < p.V) k = probe_key(load_elem<DT>(p.L, base + tid), tid);
+  if (tail0 + tid < p.V) {
+    const int v = tail0 + tid;
+    const uint64_t c = probe_key(load_elem<DT>(p.L, base + v), v);
+    k = c > k ? c : k;
+  }
+  const u32x4* vec = (const u32x4*)((const char*)p.L + (base + head) * ES);
+  constexpr int kBatch = 8;  // loads issued before any is used
+  for (int c0 = 0; c0 < nvec; c0 += kBatch * kProbeThreads) {
+    u32x4 w[kBatch];
 #pragma unroll
-    for (int q = 0; q < CPW; ++q) {
-      const int c = wave + q * kWideWaves;
-      if (c < NCMAX) dst[q] = *(const u32x4*)(wrow + (size_t)min(c, p.nchunk - 1) * KC * ESZ);
-    }
-  };
-  auto put = [&](int buf, const u32x4 (&src)[CPW]) {
+    for (int b = 0; b < kBatch; ++b) w[b] = vec[min(c0 + b * kProbeThreads + tid, max(nvec - 1, 0))];
 #pragma unroll
-    for (int q = 0; q < CPW; ++q) {
-      const int c = wave + q * kWideWaves;
-      if (c < NCMAX) tiles[buf][c][lane] = src[q];
-    }
-  };
-  // Tile t is computed from LDS buffer (t - t0) & 1 while tiles t + 1 ..
-  // t + kWideAhead are in flight in register slots: tile t0 + 1 + i + n
-  // kWideAhead sits in slot i (a W tile is 16 KB per workgroup, so one tile
-  // ahead would leave the memory system far from its bandwidth-latency
-  // product).
-  u32x4 stg[kWideAhead][CPW];
-  uint32_t lf[kWideAhead][4];
-  uint32_t l[4] = {0u, 0u, 0u, 0u};
-  fetch(t0, stg[0]);
-  if (live) load_lfrag<DT>(p, h, d, t0, l);
-  put(0, stg[0]);
+    for (int b = 0; b < kBatch; ++b) {
+      const int c = c0 + b * kProbeThreads + tid;
+      if (c < nvec) {
 #pragma unroll
-  for (int i = 0; i < kWideAhead; ++i) {
-    if (t0 + 1 + i < t1) {
-      fetch(t0 + 1 + i, stg[i]);
-      if (live) load_lfrag<DT>(p, h, d, t0 + 1 + i, lf[i]);
+        for (int e = 0; e < PER; ++e) {
+          const uint32_t word = w[b][e * ES / 4];
+          const float z = DT ? __uint_as_float((e & 1) ? (word & 0xffff0000u) : (word << 16))
+                             : __uint_as_float(word);
+          const int v = head + c * PER + e;
+          const uint64_t key = probe_key(z, v);
+          k = key > k ? key : k;
+        }
+      }
     }
   }
-  __syncthreads();
-  for (int tb = t0; tb < t1; tb += kWideAhead) {
-#pragma unroll
-    for (int i = 0; i < kWideAhead; ++i) {
-      const int t = tb + i;
-      if (t >= t1) break;
-      const int buf = (t - t0) & 1;
-      if (live) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int c = 0; c < NCMAX; ++c) acc = mfma_chunk<DT>(tiles[buf][c][lane], bfrag[c], acc);
-        tile_epilogue<DT, KMAX>(p, h, acc, l, t, h.row_ok, r);
-      }
-      if (t + 1 < t1) {
-        put(buf ^ 1, stg[i]);  // tile t + 1
-#pragma unroll
-        for (int e = 0; e < 4; ++e) l[e] = lf[i][e];
-      }
-      if (t + 1 + kWideAhead < t1) {
-        fetch(t + 1 + kWideAhead, stg[i]);
-        if (live) load_lfrag<DT>(p, h, d, t + 1 + kWideAhead, lf[i]);
-      }
-      __syncthreads();
-    }
-  }
-  if (live) publish_wave<KMAX>(p, h, slice, r);
+  return k;
 }
 
-// One workgroup per frontier row of the stage: merge the row's G slice lists
-// and (max, sum) records into its top-KMAX children and lse (lanes over
-// slices, then xor trees over the wave and the workgroup).
-template <int KMAX>
-__global__ __launch_bounds__(kMergeThreads) void rowmerge_kernel(Plan p) {
-  constexpr int NW = kMergeThreads / 64;
-  __shared__ uint64_t sh_list[NW][KMAX];
-  __shared__ float2 sh_ms[NW];
-  const int grow = blockIdx.x;
+__global__ __launch_bounds__(kProbeThreads) void probe_kernel(Plan p) {
+  constexpr int NW = kProbeThreads / 64;
+  __shared__ uint64_t best[NW * kProbeWave];
+  const int rd = blockIdx.x;  // request * B + depth
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint64_t list[KMAX];
+  uint64_t k = p.dtype ? probe_scan<1>(p, (size_t)rd * p.V) : probe_scan<0>(p, (size_t)rd * p.V);
 #pragma unroll
-  for (int i = 0; i < KMAX; ++i) list[i] = 0;
-  float m = kNegBig, s = 0.0f;
-  const uint64_t* rec = slice_record(p, 0, grow);
-  for (int g = threadIdx.x; g < p.G; g += kMergeThreads) {
-    uint64_t other[KMAX];
-    const uint64_t* src = p.part_key + ((size_t)grow * kSlicesMax + g) * KMAX;
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) other[i] = src[i];
-    list_merge(list, other);
-    lse_combine(m, s, child_key_value(rec[g]), __uint_as_float((uint32_t)rec[kHeadKeys * kSlicesMax + g]));
-  }
-#pragma unroll
-  for (int mask = 1; mask < 64; mask <<= 1) {
-    list_merge_xor(list, mask);
-    lse_combine_xor(m, s, mask);
-  }
-  if (lane == 0) {
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) sh_list[wave][i] = list[i];
-    sh_ms[wave] = make_float2(m, s);
+  for (int i = 0; i < kProbeWave; ++i) {
+    const uint64_t m = wave_max_u64(k);
+    if (k == m) k = 0;  // keys are unique: one lane gives its key up
+    if (lane == 0) best[wave * kProbeWave + i] = m;
   }
   __syncthreads();
-  if (wave == 0) {
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) list[i] = lane < NW ? sh_list[lane][i] : 0;
-    m = lane < NW ? sh_ms[lane].x : kNegBig;
-    s = lane < NW ? sh_ms[lane].y : 0.0f;
-#pragma unroll
-    for (int mask = 1; mask < NW; mask <<= 1) {
-      list_merge_xor(list, mask);
-      lse_combine_xor(m, s, mask);
+  // the kProbe best keys at their ranks; slots past the keys found (few
+  // tokens reach few waves) hold -1 and are no probe
+  __shared__ int toks[kProbe];
+  if (threadIdx.x < NW * kProbeWave) {
+    const uint64_t key = best[threadIdx.x];
+    const int rank = count_greater(best, NW * kProbeWave, key);
+    const int found = count_greater(best, NW * kProbeWave, 0ull);
+    if (key != 0 && rank < kProbe) toks[rank] = 0x7FFFFFFF - (int)(uint32_t)key;
+    if (threadIdx.x >= found && threadIdx.x < kProbe) toks[threadIdx.x] = -1;
+  }
+  __syncthreads();
+  // their tokens, W rows (zero rows for missing probes) and base logits,
+  // gathered once for the bounds of this (request, depth)
+  const int words = p.r * (p.dtype ? 2 : 4) / 4;
+  if (threadIdx.x < kProbe) {
+    const int t = toks[threadIdx.x];
+    p.probe_tok[(size_t)rd * kProbe + threadIdx.x] = t;
+    p.probe_l[(size_t)rd * kProbe + threadIdx.x] =
+        t < 0 ? 0.0f : (p.dtype ? load_elem<1>(p.L, (size_t)rd * p.V + t)
+                                : load_elem<0>(p.L, (size_t)rd * p.V + t));
+  }
+  uint32_t* dst = (uint32_t*)p.probe_w + (size_t)rd * kProbe * words;
+  for (int e = threadIdx.x; e < kProbe * words; e += blockDim.x) {
+    const int q = e / words, j = e - q * words;
+    const int t = toks[q];
+    dst[e] = t < 0 ? 0u : ((const uint32_t*)p.Wt)[(size_t)t * words + j];
+  }
+}
+
+// LDS of the per-request select kernels beyond the selection: the next
+// stage's head input rows (32-bit words) and the probe logits.
+constexpr int kProbeRowWords = 256 + 4;  // a W row of at most 1 KB, padded by 16 bytes
+
+struct NextShared {
+  // the request's selection state: a copy of its workspace entries
+  int front_node[kNarrowRows], front_tok[kNarrowRows];
+  float front_score[kNarrowRows];
+  __attribute__((aligned(16))) uint64_t top_key[PCTREE_EMIT_MAX_N];
+  int top_node[PCTREE_EMIT_MAX_N];
+  // the next stage's depth feature and probes, fetched before they are needed
+  __attribute__((aligned(16))) float h[PCTREE_MAX_RANK_BF16];
+  __attribute__((aligned(16))) uint32_t pw[kProbe * kProbeRowWords];
+  float pl[kProbe];
+  int pt[kProbe];
+  // the next stage's head input rows and probe logits
+  __attribute__((aligned(16))) uint32_t u[kNarrowRows * 256];  // rows of at most 1 KB
+  float zl[kNarrowRows * kProbe], al[kNarrowRows * kProbe];
+};
+
+// Loads of a request's select kernel that do not depend on the stage's
+// rows, issued first so that they land while the rows merge: the request's
+// selection state (frontier, running top-N) and the next stage's depth
+// feature, probe tokens, probe W rows and probe base logits.  All threads
+// call it; the caller synchronises before using nx.
+__device__ void tail_prefetch(const Plan& p, int d, int req, NextShared& nx) {
+  const int tid = threadIdx.x, nth = blockDim.x;
+  for (int i = tid; i < p.kk; i += nth) {
+    nx.front_node[i] = p.front_node[req * p.kk + i];
+    nx.front_tok[i] = p.front_tok[req * p.kk + i];
+    nx.front_score[i] = p.front_score[req * p.kk + i];
+  }
+  for (int i = tid; i < p.N; i += nth) {
+    nx.top_key[i] = p.top_key[(size_t)req * p.N + i];
+    nx.top_node[i] = p.top_node[(size_t)req * p.N + i];
+  }
+  if (d + 1 < p.B) {
+    const float* hrow = p.h + ((size_t)req * p.B + d + 1) * p.r;
+    for (int j = tid; j < p.r; j += nth) nx.h[j] = hrow[j];
+    if (stage_wide(p.mode, d + 1, p.R, p.kk) && !p.unbounded) {
+      const size_t pb = ((size_t)req * p.B + d + 1) * kProbe;
+      if (tid < kProbe) {
+        nx.pt[tid] = p.probe_tok[pb + tid];
+        nx.pl[tid] = p.probe_l[pb + tid];
+      }
+      const int words = p.r * (p.dtype ? 2 : 4) / 4;
+      const uint32_t* src = (const uint32_t*)p.probe_w + pb * words;
+      for (int e = tid; e < kProbe * words; e += nth) {
+        const int q = e / words;
+        nx.pw[q * kProbeRowWords + (e - q * words)] = src[e];
+      }
     }
-    if (lane == 0) {
+  }
+}
+
+// The request's selection state back to the workspace after its stage.
+__device__ void tail_writeback(const Plan& p, int req, const NextShared& nx) {
+  const int tid = threadIdx.x, nth = blockDim.x;
+  for (int i = tid; i < p.kk; i += nth) {
+    p.front_node[req * p.kk + i] = nx.front_node[i];
+    p.front_tok[req * p.kk + i] = nx.front_tok[i];
+    p.front_score[req * p.kk + i] = nx.front_score[i];
+  }
+  for (int i = tid; i < p.N; i += nth) {
+    p.top_key[(size_t)req * p.N + i] = nx.top_key[i];
+    p.top_node[(size_t)req * p.N + i] = nx.top_node[i];
+  }
+}
+
+// Head input of the P rows of request `req` at stage d into p.U and into
+// nx.u: u = act(E[tok] + h_d) for the rows' tokens toks[0..P) (mode 2: zero
+// rows).  Sixteen bytes of u per work item: their E and h loads are issued
+// together.  All threads of the workgroup call it.
+__device__ void next_inputs(const Plan& p, int d, int P, int req, const int* toks, NextShared& nx) {
+  const int words = p.r * (p.dtype ? 2 : 4) / 4;  // multiple of 16
+  const int units = P * (words / 4);
+  for (int e = threadIdx.x; e < units; e += blockDim.x) {
+    const int s = e / (words / 4), k = e - s * (words / 4);
+    u32x4 out = {0u, 0u, 0u, 0u};
+    if (p.mode != 2) {
+      const int tok = min(max(toks[s], 0), p.V - 1);
+      const u32x4 ev = *(const u32x4*)((const uint32_t*)p.E + (size_t)tok * words + 4 * k);
+      const float* hrow = nx.h;  // (fetched by tail_prefetch, or by the caller)
+      if (p.dtype) {
+        const f32x4 h0 = *(const f32x4*)(hrow + 8 * k), h1 = *(const f32x4*)(hrow + 8 * k + 4);
+        const float hv[8] = {h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
 #pragma unroll
-      for (int i = 0; i < KMAX; ++i) p.mrow_key[(size_t)grow * KMAX + i] = list[i];
-      p.mrow_lse[grow] = m + logf(s);
+        for (int w = 0; w < 4; ++w) {
+          const uint16_t lo = silu_bf16(__uint_as_float(ev[w] << 16), hv[2 * w]);
+          const uint16_t hi = silu_bf16(__uint_as_float(ev[w] & 0xffff0000u), hv[2 * w + 1]);
+          out[w] = (uint32_t)lo | ((uint32_t)hi << 16);
+        }
+      } else {
+        const f32x4 h0 = *(const f32x4*)(hrow + 4 * k);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) out[w] = __float_as_uint(silu_f32(__uint_as_float(ev[w]), h0[w]));
+      }
     }
+    *(u32x4*)&nx.u[s * words + 4 * k] = out;
+    *(u32x4*)((uint32_t*)p.U + ((size_t)req * p.kk + s) * words + 4 * k) = out;
+  }
+  lds_barrier();  // (the global copy is read by the next launch only)
+}
+
+// Probe logits of the P rows of request `req` at stage d on MFMA: wave w
+// (w < 2) takes probes 16 w .. 16 w + 15 as the 16 tokens of a 16x16 tile
+// (A: their W rows from memory) against the rows' head inputs in nx.u (B),
+// and the same product of absolute values for the margin.  Missing probes
+// get kNegBig.
+template <int DT>
+__device__ void probe_logits(const Plan& p, int P, NextShared& nx) {
+  constexpr int KC = DT ? 32 : 16;  // rank elements per MFMA step
+  constexpr int ESZ = DT ? 2 : 4;
+  constexpr uint32_t kAbs = DT ? 0x7FFF7FFFu : 0x7FFFFFFFu;
+  constexpr int NC = DT ? PCTREE_MAX_RANK_BF16 / 32 : PCTREE_MAX_RANK_F32 / 16;  // chunks at most
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int np = min(kProbe, p.V);
+  const int words = p.r * ESZ / 4;
+  const int q = wave * kTile + col;  // the probe this lane's A row holds
+  const uint32_t* wrow = nx.pw + min(q, kProbe - 1) * kProbeRowWords + grp * (KC / 4) * ESZ / 4;
+  const uint32_t* urow = nx.u + min(col, P - 1) * words + grp * (KC / 4) * ESZ / 4;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f}, mag = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    if (c < p.nchunk) {
+      const u32x4 a = *(const u32x4*)(wrow + c * KC * ESZ / 4);
+      u32x4 b = *(const u32x4*)(urow + c * KC * ESZ / 4);
+      if (col >= P) b = u32x4{0u, 0u, 0u, 0u};
+      acc = mfma_chunk<DT>(a, b, acc);
+      mag = mfma_chunk<DT>(a & kAbs, b & kAbs, mag);
+    }
+  }
+  // C[token 4 grp + i][row col]
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int qi = wave * kTile + 4 * grp + i;
+    if (col < P && qi < np) {
+      const bool there = nx.pt[qi] >= 0;
+      nx.zl[col * kProbe + qi] = there ? nx.pl[qi] + acc[i] : kNegBig;
+      nx.al[col * kProbe + qi] = there ? mag[i] + fabsf(nx.pl[qi]) : 0.0f;
+    }
+  }
+}
+
+// Bounds tau of the P rows of request `req` at stage d (their head inputs
+// in nx.u, the probes in nx.pw / nx.pl / nx.pt): row s gets the k'-th best
+// of its logits z = L_d + u_s . W at the probe tokens (distinct tokens, so
+// this is at most the row's k'-th best),
+// minus a margin of 1e-3 * (1 + sum |terms|), which is far above the float32
+// rounding of two r-term sums in any order; with fewer than k' probes the
+// bound is -inf.  All threads of the workgroup call it.
+__device__ void row_bounds(const Plan& p, int d, int P, int req, NextShared& nx) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nwave = blockDim.x >> 6;
+  const int np = min(kProbe, p.V);
+  if (wave < (np + kTile - 1) / kTile) {
+    if (p.dtype)
+      probe_logits<1>(p, P, nx);
+    else
+      probe_logits<0>(p, P, nx);
+  }
+  lds_barrier();
+  for (int s = wave; s < P; s += nwave) {
+    const float z = lane < np ? nx.zl[s * kProbe + lane] : kNegBig;
+    const float a = wave_max_f32(lane < np ? nx.al[s * kProbe + lane] : 0.0f);
+    int rank = 0;
+    for (int q = 0; q < np; ++q) {
+      const float o = nx.zl[s * kProbe + q];
+      rank += o > z || (o == z && q < lane);
+    }
+    if (lane < np && rank == p.kk - 1)
+      p.tau[(size_t)req * P + s] = z - 1e-3f * (1.0f + a);
+  }
+  lds_barrier();
+}
+
+// Multi-launch form: request state in the workspace, the stage-0 head input
+// and, when stage 0 runs the wide form, its rows' bounds.
+__global__ __launch_bounds__(kEmitThreads) void prologue_kernel(Plan p) {
+  __shared__ NextShared nx;
+  __shared__ int toks[1];
+  const int req = blockIdx.x;
+  const int tid = threadIdx.x;
+  init_request(p, req, tid, blockDim.x);
+  int root = p.root[req];
+  if (root < 0 || root >= p.V) root = 0;
+  if (tid == 0) {
+    p.top_key[(size_t)req * p.N] = node_key(0.0f, 0, root, 0);
+    p.top_node[(size_t)req * p.N] = 0;
+    p.front_node[req * p.kk] = 0;
+    p.front_tok[req * p.kk] = root;
+    p.front_score[req * p.kk] = 0.0f;
+    toks[0] = root;
+  }
+  tail_prefetch(p, -1, req, nx);  // depth 0's feature and probes (its state copy is unused)
+  __syncthreads();
+  next_inputs(p, 0, 1, req, toks, nx);
+  if (stage_wide(p.mode, 0, p.R, p.kk) && !p.unbounded) row_bounds(p, 0, 1, req, nx);
+}
+
+// After the rows of stage d are in ssh (top-k' children, lse): the stage
+// selection of request req (Sec. 4.1, 4.2), the next stage's head input
+// and, when the next stage runs the wide form, its rows' bounds.  P is the
+// number of head rows of stage d per request.
+__device__ void select_tail(const Plan& p, int d, int P, int req, SelShared& ssh, NextShared& nx) {
+  const int Pf = d == 0 ? 1 : p.kk;  // frontier size of stage d
+  // on the request's state copy in LDS (tail_prefetch, at the kernel's start)
+  // (the Shared-Markov and parent-independent modes: the one row of the
+  // stage serves every frontier parent of the tree)
+  const State st{nx.front_node, nx.front_tok, nx.front_score, nx.top_key, nx.top_node, req};
+  stage_select(p, st, d, Pf, req, 1, ssh, false, p.mode != 0);
+  tail_writeback(p, req, nx);
+  if (d + 1 < p.B) {
+    // next head input: the new frontier's tokens, or the greedy chain's
+    // token (Shared-Markov), or zero (parent-independent)
+    const int Pn = head_rows(p.mode, d + 1, p.kk);
+    __shared__ int toks[kNarrowRows];
+    if (threadIdx.x < Pn)
+      toks[threadIdx.x] = p.mode == 0 ? ssh.next_tok[threadIdx.x] : child_key_token(ssh.rowkeys[0][0]);
+    __syncthreads();
+    next_inputs(p, d + 1, Pn, req, toks, nx);
+    if (stage_wide(p.mode, d + 1, p.R, p.kk) && !p.unbounded) row_bounds(p, d + 1, Pn, req, nx);
   }
 }
 
@@ -2135,9 +2195,11 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, i
   __shared__ uint64_t sh_wlist[NW][KMAX];
   __shared__ float2 sh_wms[NW];
   __shared__ SelShared ssh;
+  __shared__ NextShared nx;
   const int req = blockIdx.x;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  tail_prefetch(p, d, req, nx);
 
   const int wpr = NW / P;  // waves per row
   const int prow = wave / wpr;
@@ -2187,23 +2249,476 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, i
     }
   }
   __syncthreads();
-  select_tail(p, d, P, req, ssh);
+  select_tail(p, d, P, req, ssh, nx);
 }
 
-// Rows of a stage merged by rowmerge_kernel: one WG per request reads its P
-// rows' top-k' children and lse, then the shared stage selection.
-template <int KMAX>
-__global__ __launch_bounds__(kSelectThreads) void select_merged_kernel(Plan p, int d, int P) {
-  __shared__ SelShared ssh;
-  const int req = blockIdx.x;
-  for (int e = threadIdx.x; e < P * KMAX; e += blockDim.x) {
-    const int prow = e / KMAX, i = e - prow * KMAX;
-    ssh.rowkeys[prow][i] = p.mrow_key[(size_t)(req * P + prow) * KMAX + i];
+constexpr int kWideWaves = 8;       // waves of a wide head workgroup
+constexpr int kThrRows = kWideWaves * kTile;  // rows of one column group: 8 blocks of 16
+constexpr int kThrSlots = 4;        // super-tiles (two W tiles) in the LDS ring
+
+// LDS of head_thr_kernel.  The ring slots are separate objects, so that the
+// compiler can tell the slot being loaded from the one being read (a load
+// into LDS that might alias a read would make it wait for every load in
+// flight); slot 0 also serves the exact path's list merges.
+template <int NCMAX, int KMAX>
+struct ThrShape {
+  static constexpr int kSlot = 2 * kTile * (4 * NCMAX + 1);      // u32x4: 32 padded W rows
+  static constexpr int kScratch = kWideWaves * kTile * KMAX / 2;  // u32x4 of the merges
+  static constexpr int kSlot0 = kSlot > kScratch ? kSlot : kScratch;
+};
+
+// B fragments of one frontier row (its head input; zero past the rank and
+// for rows past the stage's).
+template <int DT, int NCMAX>
+__device__ __forceinline__ void load_urow(const Plan& p, int P, int row, bool ok, int lg,
+                                          u32x4 (&b)[NCMAX]) {
+  constexpr int KC = DT ? 32 : 16;
+  constexpr int ESZ = DT ? 2 : 4;
+  const int req = ok ? row / P : 0, slot = ok ? row - req * P : 0;
+  const char* u = (const char*)p.U + ((size_t)(req * p.kk + slot) * p.r + lg * (KC / 4)) * ESZ;
+#pragma unroll
+  for (int c = 0; c < NCMAX; ++c) {
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (c < p.nchunk && ok) v = *(const u32x4*)(u + (size_t)c * KC * ESZ);
+    b[c] = v;
   }
-  for (int prow = threadIdx.x; prow < P; prow += blockDim.x)
-    ssh.lse[prow] = p.mrow_lse[req * P + prow];
+}
+
+// The careful path for one row's four logits of a tile (tokens tb .. tb+3):
+// online (max, sum of exp) with rescaling, and every logit at or above tau
+// appended to the row's candidates (a count past KMAX marks an overflow).
+template <int KMAX>
+__device__ __forceinline__ void thr_row_slow(const Plan& p, const float (&z)[4], int tb, float& m,
+                                             float& s, float tau, uint64_t* cand, int* cnt) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (tb + i < p.V) {
+      const float v = z[i];
+      if (v > m) {
+        s *= exp2_raw((m - v) * kLog2e);
+        m = v;
+      }
+      s += exp2_raw((v - m) * kLog2e);
+      if (v >= tau) {
+        const int slot = atomicAdd(cnt, 1);
+        if (slot < KMAX) cand[slot] = child_key(v, tb + i);
+      }
+    }
+  }
+}
+
+// The exact path of a slice for rows whose candidates overflowed (more than
+// KMAX at or above the bound): the slice is streamed again for those rows, 16
+// at a time, with full per-lane top-KMAX lists, and each row's KMAX best keys
+// are published.  All threads of the workgroup call it.
+template <int DT, int NCMAX, int KMAX>
+__device__ void thr_exact(const Plan& p, int d, int P, int slice, int t0, int t1, const int* ovl,
+                          int nov, uint64_t* scratch) {
+  const int wave = threadIdx.x >> 6;
+  for (int b = 0; b < nov; b += kTile) {
+    HeadLane h(p, P, 0);  // lane geometry; its row is the b + col-th listed one
+    const bool ok = b + h.col < nov;
+    const int row = ok ? ovl[b + h.col] : 0;
+    h.row = row;
+    h.row_ok = h.b_ok = ok;
+    h.req = h.b_req = row / P;
+    h.slot = h.b_slot = row - h.req * P;
+    u32x4 bf[NCMAX];
+    load_urow<DT, NCMAX>(p, P, row, ok, h.grp, bf);
+    RowAcc<KMAX> ra;
+    ra.init();
+    for (int t = t0 + wave; t < t1; t += kWideWaves) {
+      u32x4 a[NCMAX];
+      uint32_t l[4];
+      load_afrag<DT, NCMAX>(p, h, t, a);
+      load_lfrag<DT>(p, h, d, t, l);
+      tile_step<DT, NCMAX, KMAX>(p, h, a, bf, l, t, ra);
+    }
+    list_merge_pair<16>(ra.list);
+    list_merge_pair<32>(ra.list);
+    if (h.grp == 0) {
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) scratch[(i * kWideWaves + wave) * kTile + h.col] = ra.list[i];
+    }
+    __syncthreads();
+    if (wave == 0 && h.grp == 0 && ok) {
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) ra.list[i] = scratch[i * kWideWaves * kTile + h.col];
+      for (int w = 1; w < kWideWaves; ++w) {
+        uint64_t o[KMAX];
+#pragma unroll
+        for (int i = 0; i < KMAX; ++i) o[i] = scratch[(i * kWideWaves + w) * kTile + h.col];
+        list_merge(ra.list, o);
+      }
+      const size_t o = (size_t)row * kSlicesMax + slice;
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) p.part_key[o * KMAX + i] = ra.list[i];
+      p.thr_cnt[o] = KMAX;
+    }
+    __syncthreads();
+  }
+}
+
+// 16 bytes per lane from global memory straight into LDS (lane l's bytes at
+// lds_dst + 16 l), counted in vmcnt like any vector-memory load.  Issued as
+// inline assembly: the compiler does not see the LDS write, so it does not
+// make later LDS reads wait for every load in flight (it cannot tell ring
+// slots apart); the kernel orders them itself with wait_vmcnt and a
+// barrier.  M0 holds the LDS base; nothing else in the kernels that use it
+// keeps a value in M0 across it.
+__device__ __forceinline__ void load_lds16(const void* src, const void* lds_dst) {
+  const uint32_t base = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_dst);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(base)
+               : "memory", "m0");
+}
+
+// s_waitcnt with only the vector-memory count limited (gfx9 encoding:
+// vmcnt bits 3:0 and 15:14, expcnt and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// One V-slice for up to 128 frontier rows of a wide stage.  Wave w multiplies
+// tile (2 s + w / 4) of super-tile s into the two 16-row column blocks
+// 2 (w % 4) and 2 (w % 4) + 1 of its column group (their head inputs stay in
+// registers), so each W tile read from LDS serves 32 rows, and the 8 waves
+// take two tiles per step.  W goes from memory straight into a ring of
+// kThrSlots super-tiles in LDS (16 bytes per lane, already in MFMA fragment
+// order), kThrSlots - 1 super-tiles ahead, with the lanes' L_d values in a
+// register ring alongside; a step waits for its own loads (counted), then
+// for the other waves' at the barrier.  Per row the workgroup publishes its
+// slice's (max, sum of exp) and the logits at or above the row's bound tau
+// (at most KMAX; a row with more takes the exact path).  The grid has
+// 8 * ceil(G / 8) * (column groups) workgroups, XCD-ordered as in head_kernel.
+template <int DT, int NCMAX, int KMAX>
+__global__ __launch_bounds__(kWideWaves * 64) void head_thr_kernel(Plan p, int d, int P) {
+  using SH = ThrShape<NCMAX, KMAX>;
+  constexpr int KC = DT ? 32 : 16;
+  constexpr int ESZ = DT ? 2 : 4;
+  // loads per wave per super-tile: 32 rows of at most 4 NCMAX <= 64 units
+  // each, one instruction per row, over the 8 waves
+  constexpr int CPW = 2 * kTile / kWideWaves;
+  static_assert(4 * NCMAX <= 64, "a W row must fit one load instruction");
+  constexpr int LW = DT ? 2 : 4;     // 32-bit words of L_d per row and tile per lane
+  constexpr int GROUP = CPW + 2;     // vector-memory instructions per super-tile per wave
+  typedef uint32_t lvec __attribute__((ext_vector_type(LW)));
+  __shared__ u32x4 ring0[SH::kSlot0], ring1[SH::kSlot], ring2[SH::kSlot], ring3[SH::kSlot];
+  __shared__ uint64_t cand[kThrRows * KMAX];  // each row's candidates
+  __shared__ int ccnt[kThrRows];              // their count (past KMAX: overflow)
+  __shared__ float2 msx[kThrRows];            // the second wave's row statistics
+  __shared__ int ovl[kThrRows + 1];           // rows for the exact path, and their count
+  // (a switch over a constant after unrolling: the objects stay distinct)
+  auto slot_ptr = [&](int slot) -> u32x4* {
+    switch (slot) {
+      case 0: return ring0;
+      case 1: return ring1;
+      case 2: return ring2;
+      default: return ring3;
+    }
+  };
+
+  const int rows = p.R * P;
+  const int ncb = (rows + kTile - 1) / kTile;
+  const int ngrp = (ncb + kWideWaves - 1) / kWideWaves;
+  const int x = blockIdx.x & 7, jb = blockIdx.x >> 3;
+  const int grp = jb % ngrp;
+  const int slice = (jb / ngrp) * 8 + x;
+  if (slice >= p.G) return;  // the whole workgroup
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int pair = wave & 3, half = wave >> 2;
+  const int col = lane & 15, lg = lane >> 4;
+  const int row0 = grp * kThrRows;
+  const int lr0 = 2 * pair * kTile + col, lr1 = lr0 + kTile;  // rows within the group
+  const int gr0 = row0 + lr0, gr1 = row0 + lr1;
+  const bool ok0 = gr0 < rows, ok1 = gr1 < rows;
+  const bool live = row0 + 2 * pair * kTile < rows;  // the wave has a row to compute
+  const int q0 = ok0 ? gr0 / P : 0, q1 = ok1 ? gr1 / P : 0;  // requests of the two rows
+
+  for (int i = tid; i < kThrRows; i += blockDim.x) ccnt[i] = 0;
+  if (tid == 0) ovl[kThrRows] = 0;
+
+  // per row: bound, running max and sum; thr = min(tau, m) decides the careful
+  // path (rows past the stage's never take it)
+  const float big = 3.0e38f;
+  float tau0 = ok0 ? (p.unbounded ? kNegBig : p.tau[gr0]) : big;
+  float tau1 = ok1 ? (p.unbounded ? kNegBig : p.tau[gr1]) : big;
+  float m0 = ok0 ? tau0 : kNegBig, s0 = 0.0f;
+  float m1 = ok1 ? tau1 : kNegBig, s1 = 0.0f;
+  float thr0 = ok0 ? fminf(tau0, m0) : big, thr1 = ok1 ? fminf(tau1, m1) : big;
+
+  const int t0 = slice * p.tiles_per_slice;
+  const int t1 = min(t0 + p.tiles_per_slice, p.ntiles);
+  const int nsup = (t1 - t0 + 1) / 2;
+  const int ru = p.r * ESZ / 16;  // 16-byte units of a W row (a multiple of 4, at most 64)
+  const char* lrow0 = (const char*)p.L + ((size_t)q0 * p.B + d) * p.V * ESZ;
+  const char* lrow1 = (const char*)p.L + ((size_t)q1 * p.B + d) * p.V * ESZ;
+  // whether 16-bit L_d rows allow one aligned vector load of four tokens
+  const bool lvec_ok = ((size_t)p.V * ESZ) % (LW * 4) == 0;
+
+  // One super-tile's loads: its 32 token rows of W straight into its ring
+  // slot, one row per instruction (lane l loads the row's l-th 16 bytes, so
+  // an instruction reads one contiguous run), then the lane's L_d words for
+  // both rows.  In the slot, row i starts at unit i (ru + 1): the one unit of
+  // padding puts the 16 rows of an MFMA A-fragment read (one unit each) in 16
+  // different bank groups.  Tokens past the slice or V re-read the last one.
+  // (slot == s % kThrSlots, passed as a constant of the unrolled loops)
+  auto issue = [&](int s, int slot, lvec (&l)[2]) {
+#pragma unroll
+    for (int q = 0; q < CPW; ++q) {
+      const int row = wave + q * kWideWaves;  // token row of the super-tile
+      const int t = min(t0 + 2 * s + row / kTile, t1 - 1);
+      const int tok = min(t * kTile + (row & (kTile - 1)), p.V - 1);
+      const char* src = (const char*)p.Wt + (size_t)tok * p.r * ESZ + (size_t)min(lane, ru - 1) * 16;
+      if (lane < ru) load_lds16(src, slot_ptr(slot) + row * (ru + 1));
+    }
+    const int t = min(t0 + 2 * s + half, t1 - 1);
+    const int tb = min(t * kTile + lg * 4, p.V - 4 > 0 ? p.V - 4 : 0);
+    if (lvec_ok && p.V >= 4) {
+      l[0] = *(const lvec*)(lrow0 + (size_t)tb * ESZ);
+      l[1] = *(const lvec*)(lrow1 + (size_t)tb * ESZ);
+    } else {  // (unaligned rows: word by word, still two vector-memory instructions' worth)
+      lvec a, b;
+#pragma unroll
+      for (int i = 0; i < LW; ++i) { a[i] = 0u; b[i] = 0u; }
+      const int tb2 = t * kTile + lg * 4;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int v = min(tb2 + i, p.V - 1);
+        const uint32_t ra = load_raw<DT>(p.L, ((size_t)q0 * p.B + d) * p.V + v);
+        const uint32_t rb = load_raw<DT>(p.L, ((size_t)q1 * p.B + d) * p.V + v);
+        if (DT) {
+          a[i / 2] |= ra << (16 * (i & 1));
+          b[i / 2] |= rb << (16 * (i & 1));
+        } else {
+          a[i] = ra;
+          b[i] = rb;
+        }
+      }
+      l[0] = a;
+      l[1] = b;
+    }
+  };
+  // the four L_d values of the lane's tokens (tokens tb .. tb + 3 of its
+  // tile, realigned when the vector load had to start earlier)
+  auto lval = [&](const lvec& l, int tb, int i) -> float {
+    const int shift = (lvec_ok && p.V >= 4) ? tb - min(tb, p.V - 4 > 0 ? p.V - 4 : 0) : 0;
+    const int e = min(i + shift, 3);
+    return DT ? __uint_as_float((e & 1) ? (l[e / 2] & 0xffff0000u) : (l[e / 2] << 16))
+              : __uint_as_float(l[e]);
+  };
+
+  // the first super-tiles' loads, then the head inputs of the wave's rows
+  // (B fragments, in flight behind them), then one wait for everything: the
+  // candidate counts are zero for every wave before any appends (the ring's
+  // barriers below do not wait for LDS stores), and the ring's counted waits
+  // start from an empty queue
+  lvec lring[kThrSlots][2];
+#pragma unroll
+  for (int i = 0; i + 1 < kThrSlots; ++i)
+    if (i < nsup) issue(i, i, lring[i]);
+  u32x4 b0[NCMAX], b1[NCMAX];
+  load_urow<DT, NCMAX>(p, P, gr0, ok0 && live, lg, b0);
+  load_urow<DT, NCMAX>(p, P, gr1, ok1 && live, lg, b1);
   __syncthreads();
-  select_tail(p, d, P, req, ssh);
+
+  for (int sb = 0; sb < nsup; sb += kThrSlots) {
+#pragma unroll
+    for (int i = 0; i < kThrSlots; ++i) {
+      const int s = sb + i;
+      if (s >= nsup) break;
+      // this wave's loads of super-tile s (and of its L_d words) have landed
+      // once at most the later super-tiles' loads are outstanding
+      if (s + 2 < nsup)
+        wait_vmcnt<2 * GROUP>();
+      else if (s + 1 < nsup)
+        wait_vmcnt<GROUP>();
+      else
+        wait_vmcnt<0>();
+      // and every wave's: ring slot s is complete, slot s - 1 is free
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      __builtin_amdgcn_s_barrier();
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      if (s + kThrSlots - 1 < nsup)
+        issue(s + kThrSlots - 1, (i + kThrSlots - 1) % kThrSlots,
+              lring[(i + kThrSlots - 1) % kThrSlots]);
+      const int t = t0 + 2 * s + half;
+      if (live && t < t1) {
+        f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+        // lane: token col of tile `half`, units c * 4 + lg (chunks past the
+        // rank re-read the last one: finite values that meet zero B fragments)
+        const u32x4* a = slot_ptr(i) + (half * kTile + col) * (ru + 1) + lg;  // (s % kThrSlots == i)
+#pragma unroll
+        for (int c = 0; c < NCMAX; ++c) {
+          const u32x4 av = a[min(c, p.nchunk - 1) * 4];
+          c0 = mfma_chunk<DT>(av, b0[c], c0);
+          c1 = mfma_chunk<DT>(av, b1[c], c1);
+        }
+        const int tb = t * kTile + lg * 4;
+        float z0[4], z1[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          z0[e] = c0[e] + lval(lring[i][0], tb, e);
+          z1[e] = c1[e] + lval(lring[i][1], tb, e);
+        }
+        const float mx0 = fmaxf(fmaxf(z0[0], z0[1]), fmaxf(z0[2], z0[3]));
+        const float mx1 = fmaxf(fmaxf(z1[0], z1[1]), fmaxf(z1[2], z1[3]));
+        // the careful path: a logit at or above the bound or the running
+        // maximum, or tokens past V (only in the vocabulary's last tile)
+        const bool hot = mx0 >= thr0 || mx1 >= thr1 || tb + 3 >= p.V;
+        if (__builtin_expect(__any(hot), 0)) {
+          if (ok0) thr_row_slow<KMAX>(p, z0, tb, m0, s0, tau0, cand + lr0 * KMAX, ccnt + lr0);
+          if (ok1) thr_row_slow<KMAX>(p, z1, tb, m1, s1, tau1, cand + lr1 * KMAX, ccnt + lr1);
+          thr0 = ok0 ? fminf(tau0, m0) : big;
+          thr1 = ok1 ? fminf(tau1, m1) : big;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            s0 += exp2_raw((z0[e] - m0) * kLog2e);
+            s1 += exp2_raw((z1[e] - m1) * kLog2e);
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();  // the ring is free for the exact path; candidates complete
+
+  // the row statistics: the four lane groups, then the two waves of a row
+  lse_combine_pair<16>(m0, s0);
+  lse_combine_pair<32>(m0, s0);
+  lse_combine_pair<16>(m1, s1);
+  lse_combine_pair<32>(m1, s1);
+  if (half == 1 && lg == 0) {
+    msx[lr0] = make_float2(m0, s0);
+    msx[lr1] = make_float2(m1, s1);
+  }
+  __syncthreads();
+  if (half == 0 && lg == 0) {
+    if (ok0) {
+      lse_combine(m0, s0, msx[lr0].x, msx[lr0].y);
+      *(float2*)(p.thr_ms + ((size_t)gr0 * kSlicesMax + slice) * 2) = make_float2(m0, s0);
+    }
+    if (ok1) {
+      lse_combine(m1, s1, msx[lr1].x, msx[lr1].y);
+      *(float2*)(p.thr_ms + ((size_t)gr1 * kSlicesMax + slice) * 2) = make_float2(m1, s1);
+    }
+  }
+  // the candidates: rows within KMAX publish theirs, the others are listed
+  // for the exact path
+  for (int e = tid; e < kThrRows * KMAX; e += blockDim.x) {
+    const int lr = e / KMAX, i = e - lr * KMAX;
+    const int gr = row0 + lr;
+    if (gr < rows) {
+      const int c = ccnt[lr];
+      const size_t o = (size_t)gr * kSlicesMax + slice;
+      if (c <= KMAX) {
+        if (i < c) p.part_key[o * KMAX + i] = cand[lr * KMAX + i];
+        if (i == 0) p.thr_cnt[o] = c;
+      } else if (i == 0) {
+        ovl[atomicAdd(&ovl[kThrRows], 1)] = gr;
+      }
+    }
+  }
+  __syncthreads();
+  const int nov = ovl[kThrRows];
+  if (nov > 0)
+    thr_exact<DT, NCMAX, KMAX>(p, d, P, slice, t0, t1, ovl, nov, (uint64_t*)ring0);
+}
+
+// One WG per request after a wide head stage: each of its rows (one wave per
+// row) merges the slices' (max, sum of exp) into its lse and the slices'
+// candidates into its k' children; then the stage selection, the next
+// stage's head input and its rows' bounds (select_tail).
+constexpr int kMergeCap = 256;  // candidates of a row ranked in LDS (more: list merges)
+
+template <int KMAX>
+__global__ __launch_bounds__(kSelectThreads) void mergesel_kernel(Plan p, int d, int P) {
+  __shared__ SelShared ssh;
+  __shared__ NextShared nx;
+  __shared__ __attribute__((aligned(16))) uint64_t mk[kNarrowRows][kMergeCap];
+  const int req = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // the lane's slices of its wave's row (at most kSlicesMax / 64):
+  // statistics and counts first, all loads in flight together, then the
+  // state and next-stage loads behind them, then the few candidates
+  constexpr int SPL = kSlicesMax / 64;
+  const int gr = req * P + min(wave, P - 1);
+  float2 v[SPL];
+  int c[SPL];
+  if (wave < P) {
+#pragma unroll
+    for (int i = 0; i < SPL; ++i) {
+      const int g = lane + 64 * i;
+      const size_t o = (size_t)gr * kSlicesMax + min(g, p.G - 1);
+      v[i] = *(const float2*)(p.thr_ms + o * 2);
+      c[i] = g < p.G ? min(p.thr_cnt[o], KMAX) : 0;
+    }
+  }
+  tail_prefetch(p, d, req, nx);
+  if (wave < P) {
+    float m = kNegBig, s = 0.0f;
+    int mine = 0;
+#pragma unroll
+    for (int i = 0; i < SPL; ++i) {
+      if (lane + 64 * i < p.G) lse_combine(m, s, v[i].x, v[i].y);
+      mine += c[i];
+    }
+    const float M = wave_max_f32(m);
+    const float S = wave_sum_f32(s * exp2_raw((m - M) * kLog2e));
+    // the row's candidates, gathered in LDS at the lanes' exclusive prefix sums
+    int off = mine;
+#pragma unroll
+    for (int sh = 1; sh < 64; sh <<= 1) {
+      const int o = __shfl_up(off, sh);
+      if (lane >= sh) off += o;
+    }
+    const int n = __shfl(off, 63);
+    off -= mine;
+    uint64_t* keys = mk[wave];
+    if (n <= kMergeCap) {
+#pragma unroll
+      for (int i = 0; i < SPL; ++i) {
+        const size_t o = (size_t)gr * kSlicesMax + min(lane + 64 * i, p.G - 1);
+        for (int j = 0; j < c[i]; ++j) keys[off++] = p.part_key[o * KMAX + j];
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    if (n <= kMergeCap) {
+      // rank each key among the row's (keys are unique: distinct tokens)
+      if (lane < KMAX) ssh.rowkeys[wave][lane] = 0;
+      __builtin_amdgcn_wave_barrier();
+      for (int k = lane; k < n; k += 64) {
+        const uint64_t key = keys[k];
+        const int rank = count_greater(keys, n, key);
+        if (rank < KMAX) ssh.rowkeys[wave][rank] = key;
+      }
+    } else {
+      // (many candidates: per-lane top-KMAX lists merged over the wave)
+      uint64_t lst[KMAX];
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) lst[i] = 0;
+#pragma unroll
+      for (int i = 0; i < SPL; ++i) {
+        const size_t o = (size_t)gr * kSlicesMax + min(lane + 64 * i, p.G - 1);
+        for (int j = 0; j < c[i]; ++j) {
+          const uint64_t k = p.part_key[o * KMAX + j];
+          if (k > lst[KMAX - 1]) list_insert(lst, k);
+        }
+      }
+#pragma unroll
+      for (int mask = 1; mask < 64; mask <<= 1) list_merge_xor(lst, mask);
+      if (lane == 0) {
+#pragma unroll
+        for (int i = 0; i < KMAX; ++i) ssh.rowkeys[wave][i] = lst[i];
+      }
+    }
+    if (lane == 0) ssh.lse[wave] = M + logf(S);
+  }
+  __syncthreads();
+  select_tail(p, d, P, req, ssh, nx);
 }
 
 // Zero the words the persistent round polls (slice partials of every stage,
@@ -2286,7 +2801,7 @@ typedef void (*RoundFn)(Plan);
   PCTREE_KMAX_SWITCH(KERNEL, 0, 8, (p).kmax)
 
 StageFn head_fn(const Plan& p) { PCTREE_DISPATCH(head_kernel, p) }
-StageFn head_wide_fn(const Plan& p) { PCTREE_DISPATCH(head_wide_kernel, p) }
+StageFn head_thr_fn(const Plan& p) { PCTREE_DISPATCH(head_thr_kernel, p) }
 
 // NCMAX of the instantiation PCTREE_DISPATCH picks.
 int nchunk_max(const Plan& p) {
@@ -2308,24 +2823,13 @@ RoundFn round_fn(const Plan& p) {
   PCTREE_ROUND_KMAX_SWITCH(round_kernel, 0, 8, p.kmax, fold)
 }
 
-typedef void (*MergeFn)(Plan);
-MergeFn rowmerge_fn(int kmax) {
+StageFn mergesel_fn(int kmax) {
   switch (kmax) {
-    case 1: return rowmerge_kernel<1>;
-    case 2: return rowmerge_kernel<2>;
-    case 4: return rowmerge_kernel<4>;
-    case 8: return rowmerge_kernel<8>;
-    default: return rowmerge_kernel<16>;
-  }
-}
-
-StageFn select_merged_fn(int kmax) {
-  switch (kmax) {
-    case 1: return select_merged_kernel<1>;
-    case 2: return select_merged_kernel<2>;
-    case 4: return select_merged_kernel<4>;
-    case 8: return select_merged_kernel<8>;
-    default: return select_merged_kernel<16>;
+    case 1: return mergesel_kernel<1>;
+    case 2: return mergesel_kernel<2>;
+    case 4: return mergesel_kernel<4>;
+    case 8: return mergesel_kernel<8>;
+    default: return mergesel_kernel<16>;
   }
 }
 
@@ -2447,33 +2951,37 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
     if (e != hipSuccess) return e;
     return hipGetLastError();
   }
+  p.unbounded = dbg.wide_unbounded;
+  bool any_wide = false;
+  for (int d = 0; d < p.B; ++d) any_wide = any_wide || stage_wide(p.mode, d, p.R, p.kk);
+  if (any_wide && !p.unbounded)
+    hipLaunchKernelGGL(probe_kernel, dim3(p.R * p.B), dim3(kProbeThreads), 0, st, p);
   hipLaunchKernelGGL(prologue_kernel, dim3(p.R), dim3(kEmitThreads), 0, st, p);
   const StageFn head = head_fn(p);
   const StageFn sel = select_fn(p.kmax);
-  const StageFn head_wide = head_wide_fn(p);
-  const MergeFn merge = rowmerge_fn(p.kmax);
-  const StageFn sel_merged = select_merged_fn(p.kmax);
+  const StageFn head_thr = any_wide ? head_thr_fn(p) : nullptr;
+  const StageFn mergesel = mergesel_fn(p.kmax);
   const int slices8 = (p.G + 7) / 8 * 8;
   for (int d = 0; d < p.B; ++d) {
     // head rows per request: the frontier, or the one shared row of the stage
-    const int P = (d == 0 || p.mode != 0) ? 1 : p.kk;
-    const int cb = (p.R * P + kTile - 1) / kTile;
+    const int P = head_rows(p.mode, d, p.kk);
     const bool prof = profile_on();
-    if (cb == 1) {
+    if (!stage_wide(p.mode, d, p.R, p.kk)) {
       // one column block: 4 waves split the slice's tiles; one WG per
       // request merges and selects
       if (prof) profile_mark(st, "head_kernel");
-      hipLaunchKernelGGL(head, dim3(slices8 * cb), dim3(kHeadThreads), 0, st, p, d, P);
+      hipLaunchKernelGGL(head, dim3(slices8), dim3(kHeadThreads), 0, st, p, d, P);
       if (prof) profile_mark(st, "head_kernel");
       hipLaunchKernelGGL(sel, dim3(p.R), dim3(kSelectThreads), 0, st, p, d, P);
     } else {
-      // wide: 8 column blocks share each W tile; rows merge in parallel
+      // wide: up to 128 rows per workgroup, bounded candidates; one WG per
+      // request merges its rows and selects
+      const int cb = (p.R * P + kTile - 1) / kTile;
       const int ngrp = (cb + kWideWaves - 1) / kWideWaves;
-      if (prof) profile_mark(st, "head_wide_kernel");
-      hipLaunchKernelGGL(head_wide, dim3(slices8 * ngrp), dim3(kWideWaves * 64), 0, st, p, d, P);
-      if (prof) profile_mark(st, "head_wide_kernel");
-      hipLaunchKernelGGL(merge, dim3(p.R * P), dim3(kMergeThreads), 0, st, p);
-      hipLaunchKernelGGL(sel_merged, dim3(p.R), dim3(kSelectThreads), 0, st, p, d, P);
+      if (prof) profile_mark(st, "head_thr_kernel");
+      hipLaunchKernelGGL(head_thr, dim3(slices8 * ngrp), dim3(kWideWaves * 64), 0, st, p, d, P);
+      if (prof) profile_mark(st, "head_thr_kernel");
+      hipLaunchKernelGGL(mergesel, dim3(p.R), dim3(kSelectThreads), 0, st, p, d, P);
     }
   }
   hipLaunchKernelGGL(emit_kernel, dim3(p.R), dim3(kEmitThreads), 0, st, p);

@@ -18,6 +18,7 @@ constexpr int kMaskThreads = 256;
 constexpr int kRoundWaves = 8;       // waves per WG of the persistent round kernel
 constexpr int kNarrowRows = 16;      // frontier rows (R * k') one column block holds
 constexpr int kFlagStride = 64;      // ints between two workgroups' flag words (256 B)
+constexpr int kProbe = 32;           // probe tokens per (request, depth) of the wide stages
 
 // What a streaming workgroup publishes per (stage, row, slice) besides its
 // candidate list, the slice record: kRecWords 64-bit words, the list's
@@ -79,10 +80,15 @@ struct Plan {
   uint64_t* part_hd; // [stages][rows_max][kRecWords][kSlicesMax] slice records
   int* req_bad;      // [R] root token outside [0, V)
   uint64_t* front_w; // [stages][rows_max] frontier of each stage (persistent form)
-  uint64_t* mrow_key;// [rows_max][kmax] merged top-k' children of each row (wide stages)
-  float* mrow_lse;   // [rows_max] merged lse of each row (wide stages)
+  float* tau;        // [rows_max] wide stages: lower bound of each row's k'-th best logit
+  int* probe_tok;    // [R][B][kProbe] wide stages: probe tokens of each request and depth
+  void* probe_w;     // [R][B][kProbe][r] (dtype) their W rows (zero for a missing probe)
+  float* probe_l;    // [R][B][kProbe] their base logits L_d
+  float* thr_ms;     // [rows_max][kSlicesMax][2] wide stages: each slice's (max, sum of exp)
+  int* thr_cnt;      // [rows_max][kSlicesMax] wide stages: candidates each slice kept
   uint32_t tag;      // this call's tag, 1 .. kTagMask (published words carry it)
   int mode;          // 0 parent-conditioned, 1 Shared-Markov, 2 parent-independent
+  int unbounded;     // wide stages ignore tau (every logit is a candidate)
   long long spin_ticks;  // device wall-clock ticks a wait may last before aborting
   int lds_tiles;         // W tiles a streaming block keeps in LDS for the whole round
   int lds_top_offset;    // byte offset of the keeper's running top-N in the dynamic LDS
@@ -105,6 +111,7 @@ struct DebugConfig {
   long long wait_ticks = -1;  // < 0: 2 s of device wall clock per bounded wait
   int force_multilaunch = 0;  // nonzero: per-stage launches even for narrow rounds
   int round_slices = 0;       // > 0: V-slices of the persistent round (else one per CU but one)
+  int wide_unbounded = 0;     // nonzero: wide stages without their per-row bound
 };
 DebugConfig& debug_config();
 

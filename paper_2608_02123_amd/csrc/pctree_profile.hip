@@ -88,6 +88,7 @@ pctree_status pctree_debug_set(const pctree_debug_config* cfg) {
     d.wait_ticks = cfg->wait_ticks < 0 ? -1 : (long long)cfg->wait_ticks;
     d.force_multilaunch = cfg->force_multilaunch != 0;
     d.round_slices = cfg->round_slices;
+    d.wide_unbounded = cfg->wide_unbounded != 0;
   }
   debug_config() = d;
   return PCTREE_OK;

@@ -90,7 +90,7 @@ class _Trace(ctypes.Structure):
 class DebugConfig(ctypes.Structure):
     """pctree_debug_config of include/pctree_profile.h (test-only launch overrides)."""
     _fields_ = [("wait_ticks", ctypes.c_int64), ("force_multilaunch", ctypes.c_int32),
-                ("round_slices", ctypes.c_int32)]
+                ("round_slices", ctypes.c_int32), ("wide_unbounded", ctypes.c_int32)]
 
 
 _lib = None
@@ -317,9 +317,10 @@ def build_tree(L, E, Wt, h, root, prefix_len, k, N, *, mask=True, trace=False, s
 
 
 def debug_set(wait_ticks: int = -1, force_multilaunch: bool = False,
-              round_slices: int = 0) -> None:
+              round_slices: int = 0, wide_unbounded: bool = False) -> None:
     """Test-only launch overrides (pctree_debug_set); no arguments restores the defaults."""
-    cfg = DebugConfig(int(wait_ticks), 1 if force_multilaunch else 0, int(round_slices))
+    cfg = DebugConfig(int(wait_ticks), 1 if force_multilaunch else 0, int(round_slices),
+                      1 if wide_unbounded else 0)
     _check(lib().pctree_debug_set(ctypes.byref(cfg)), "pctree_debug_set")
 
 

@@ -83,8 +83,8 @@ def test_abandoned_counts_raise():
 
 
 def test_debug_set_validates_and_restores():
-    bad = P.DebugConfig(-1, 0, -5)
+    bad = P.DebugConfig(-1, 0, -5, 0)
     assert P.lib().pctree_debug_set(ctypes.byref(bad)) == P.ERR_INVALID_ARGUMENT
-    P.debug_set(wait_ticks=0, force_multilaunch=True, round_slices=7)
+    P.debug_set(wait_ticks=0, force_multilaunch=True, round_slices=7, wide_unbounded=True)
     assert P.lib().pctree_debug_set(None) == P.OK
     P.debug_set()

@@ -97,3 +97,37 @@ def test_abandoned_round_pads_every_output_then_recovers():
         assert torch.equal(again[key], good[key]), f"{key} differs after the abandoned round"
     reps = C.compare_batch(again, inp, w.k, w.N, label="qwen4b_b7/after abort")
     assert reps[0]["exact"]
+
+
+WIDE = [
+    # V, B, N, k, r, R, dtype: more than 16 frontier rows per stage
+    (2000, 3, 48, 16, 64, 2, "bf16"),
+    (3000, 4, 40, 8, 128, 5, "f32"),
+    (700, 3, 30, 5, 32, 9, "bf16"),
+    (9000, 3, 64, 16, 512, 3, "bf16"),
+]
+
+
+@pytest.mark.parametrize("shape", WIDE, ids=lambda s: "V{}B{}N{}k{}r{}R{}{}".format(*s))
+def test_wide_stages_without_row_bounds(shape):
+    """Wide stages with their per-row bounds switched off: every logit is a
+    candidate, every (row, slice) overflows its candidate slots and takes the
+    exact per-slice path.  The tree must equal the bounded run's and the
+    oracle's."""
+    from paper_2608_02123_amd.synth import Workload
+
+    V, B, N, k, r, R, dt = shape
+    w = Workload("wu", V=V, B=B, N=N, k=k, r=r, R=R, dtype=dt, peak="uniform", seed=9)
+    inp = make_inputs(w)
+    dev = P.device_inputs(inp)
+    b = _builder(w)
+    say(f"[launch] wide {shape}: bounded")
+    ref = _run(b, dev)
+    say(f"[launch] wide {shape}: unbounded (exact path everywhere)")
+    out = _run(b, dev, wide_unbounded=True)
+    reps = C.compare_batch(out, inp, k, N, label=f"wide unbounded {shape}")
+    for key in TREE_KEYS:
+        assert torch.equal(out[key], ref[key]), f"{key} differs between bounded and unbounded"
+    np.testing.assert_allclose(out["logprob"].cpu().numpy(), ref["logprob"].cpu().numpy(),
+                               atol=C.SCORE_GUARD)
+    assert all(r_["exact"] or r_["identical"] for r_ in reps)

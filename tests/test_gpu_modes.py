@@ -41,6 +41,7 @@ SHAPES = [
     (1000, 3, 40, 16, 32, 3, "bf16"),  # max k, three requests
     (3000, 6, 33, 1, 96, 4, "bf16"),   # k = 1: the chain itself
     (300, 63, 256, 2, 32, 1, "bf16"),  # max depth and budget
+    (700, 3, 30, 5, 32, 20, "bf16"),   # 20 requests: every stage runs the wide form
 ]
 
 
