@@ -34,6 +34,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <type_traits>
 
 #define PCTREE_EMIT_MAX_N 256
 #define PCTREE_MASK_MAX_N 1024
@@ -1226,6 +1227,34 @@ __device__ __forceinline__ int count_greater(const uint64_t* keys, int n, uint64
   return cnt;
 }
 
+// The same count by a group of T adjacent lanes (T a power of two <= 64):
+// lane q of the group counts keys q, q + T, q + 2T, ... (the group reads T
+// consecutive keys per load, no bank conflicts), eight loads in flight at a
+// time, and the group adds its counts over lane swaps.  Every lane of the
+// wave must call it (n = 0 for lanes without a key); each lane gets the
+// group's count.
+__device__ __forceinline__ int count_greater_group(const uint64_t* keys, int n, uint64_t key,
+                                                   int q, int T) {
+  int cnt = 0;
+  for (int b = q; b < n; b += 8 * T) {
+    uint64_t v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = keys[min(b + i * T, n - 1)];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cnt += (b + i * T < n) & (v[i] > key);
+  }
+  for (int m = 1; m < T; m <<= 1) cnt += __shfl_xor(cnt, m);
+  return cnt;
+}
+
+// Lanes per key for count_greater_group: the largest power of two <= 64
+// with n keys * T <= nthreads.
+__device__ __forceinline__ int group_lanes(int n, int nthreads) {
+  int T = 1;
+  while (T < 64 && n * T * 2 <= nthreads) T *= 2;
+  return T;
+}
+
 struct SelShared {
   int next_tok[kNarrowRows];  // tokens of the next frontier, by slot (request-major)
   uint64_t rowkeys[kNarrowRows][16];  // top-k' children (child keys) of each row
@@ -1241,10 +1270,16 @@ struct SelShared {
 // request req0's slot 0): score them (Eq. 4), put them into the pool, pick the
 // next frontier (the k' best of each request's layer, Sec. 4.1), merge them
 // into the running global top-N (Sec. 4.2) and write the next head input.
-// Needs blockDim >= 512 and nreq * P * k' <= 256.
+// Needs blockDim >= 512 and nreq * P * k' <= 256.  `mid` runs (all threads)
+// once the next frontier is in sh.next_tok and the pool entries are stored,
+// before the top-N merge: a caller issues the next stage's loads there.
+struct NoMid {
+  __device__ void operator()() const {}
+};
+template <class Mid = NoMid>
 __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st, int d, int P,
                                                   int req0, int nreq, SelShared& sh,
-                                                  bool bcast, bool shared) {
+                                                  bool bcast, bool shared, Mid mid = Mid()) {
   const int tid = threadIdx.x;
   const int kk = p.kk;
   const int per_req = P * kk;
@@ -1273,10 +1308,15 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
   // (the frontier's loads above have returned: LDS barriers suffice until
   // the frontier is rewritten)
   lds_barrier();
-  // rank within the request's layer
-  if (tid < ncand) {
-    const int rq = tid / per_req;
-    sh.rank[tid] = count_greater(sh.ckey + rq * per_req, per_req, sh.ckey[tid]);
+  // rank within the request's layer, T lanes per candidate
+  {
+    const int T = group_lanes(ncand, blockDim.x);
+    const int c = tid / T;
+    const bool live = c < ncand;
+    const int rq = live ? c / per_req : 0;
+    const int cnt = count_greater_group(sh.ckey + rq * per_req, live ? per_req : 0,
+                                        live ? sh.ckey[c] : 0, tid & (T - 1), T);
+    if (live && (tid & (T - 1)) == 0) sh.rank[c] = cnt;
   }
   lds_barrier();
   // next frontier (every frontier slot was read above, before the barriers)
@@ -1310,6 +1350,7 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
     p.node_depth[id] = d + 1;
     p.node_score[id] = score;
   }
+  mid();
   // running global top-N, one request at a time: every element's new
   // position is its rank in the union (both sides are sorted), computed
   // before any element moves.  The state is in LDS (every caller keeps a
@@ -1342,7 +1383,10 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
       tn[pos] = node;
     }
   }
-  __syncthreads();
+  // (the stage's global stores, pool entries and trace, are read by later
+  // launches or, in the persistent form, by the emission after a full
+  // barrier: an LDS barrier ends the stage)
+  lds_barrier();
 }
 
 // The stage, init and emission routines have an out-of-line entry (used by the
@@ -1827,6 +1871,7 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
     else
       stage_select(p, st, d, P, 0, p.R, ssh, true);
   }
+  __syncthreads();  // the pool entries stored by the stages are visible to every wave
   for (int req = 0; req < p.R; ++req) {
     if constexpr (kInline)
       emit_request_body(p, st, req);
@@ -1979,7 +2024,8 @@ struct NextShared {
   int pt[kProbe];
   // the next stage's head input rows and probe logits
   __attribute__((aligned(16))) uint32_t u[kNarrowRows * 256];  // rows of at most 1 KB
-  float zl[kNarrowRows * kProbe], al[kNarrowRows * kProbe];
+  __attribute__((aligned(16))) float zl[kNarrowRows * kProbe];
+  float al[kNarrowRows * kProbe];
 };
 
 // Loads of a request's select kernel that do not depend on the stage's
@@ -2035,15 +2081,31 @@ __device__ void tail_writeback(const Plan& p, int req, const NextShared& nx) {
 // nx.u: u = act(E[tok] + h_d) for the rows' tokens toks[0..P) (mode 2: zero
 // rows).  Sixteen bytes of u per work item: their E and h loads are issued
 // together.  All threads of the workgroup call it.
-__device__ void next_inputs(const Plan& p, int d, int P, int req, const int* toks, NextShared& nx) {
+__device__ __forceinline__ u32x4 next_e_unit(const Plan& p, int e, const int* toks) {
+  const int words = p.r * (p.dtype ? 2 : 4) / 4;
+  const int s = e / (words / 4), k = e - s * (words / 4);
+  const int tok = min(max(toks[s], 0), p.V - 1);
+  return *(const u32x4*)((const uint32_t*)p.E + (size_t)tok * words + 4 * k);
+}
+
+// The E bytes of the thread's first unit of next_inputs, loaded ahead (zero
+// when the thread has none, or in mode 2).
+__device__ __forceinline__ u32x4 next_e_first(const Plan& p, int P, const int* toks) {
+  const int units = P * (p.r * (p.dtype ? 2 : 4) / 16);
+  return p.mode != 2 && (int)threadIdx.x < units ? next_e_unit(p, threadIdx.x, toks)
+                                                 : u32x4{0u, 0u, 0u, 0u};
+}
+
+// (first: the thread's first unit's E bytes from next_e_first, or null)
+__device__ void next_inputs(const Plan& p, int d, int P, int req, const int* toks, NextShared& nx,
+                            const u32x4* first = nullptr) {
   const int words = p.r * (p.dtype ? 2 : 4) / 4;  // multiple of 16
   const int units = P * (words / 4);
   for (int e = threadIdx.x; e < units; e += blockDim.x) {
     const int s = e / (words / 4), k = e - s * (words / 4);
     u32x4 out = {0u, 0u, 0u, 0u};
     if (p.mode != 2) {
-      const int tok = min(max(toks[s], 0), p.V - 1);
-      const u32x4 ev = *(const u32x4*)((const uint32_t*)p.E + (size_t)tok * words + 4 * k);
+      const u32x4 ev = first && e == (int)threadIdx.x ? *first : next_e_unit(p, e, toks);
       const float* hrow = nx.h;  // (fetched by tail_prefetch, or by the caller)
       if (p.dtype) {
         const f32x4 h0 = *(const f32x4*)(hrow + 8 * k), h1 = *(const f32x4*)(hrow + 8 * k + 4);
@@ -2085,14 +2147,25 @@ __device__ void probe_logits(const Plan& p, int P, NextShared& nx) {
   const uint32_t* wrow = nx.pw + min(q, kProbe - 1) * kProbeRowWords + grp * (KC / 4) * ESZ / 4;
   const uint32_t* urow = nx.u + min(col, P - 1) * words + grp * (KC / 4) * ESZ / 4;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f}, mag = {0.f, 0.f, 0.f, 0.f};
+  // four chunks' fragments loaded together per step (chunks past the rank
+  // re-read the last one with a zero B fragment)
+  constexpr int CB = 4;
 #pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    if (c < p.nchunk) {
-      const u32x4 a = *(const u32x4*)(wrow + c * KC * ESZ / 4);
-      u32x4 b = *(const u32x4*)(urow + c * KC * ESZ / 4);
-      if (col >= P) b = u32x4{0u, 0u, 0u, 0u};
-      acc = mfma_chunk<DT>(a, b, acc);
-      mag = mfma_chunk<DT>(a & kAbs, b & kAbs, mag);
+  for (int c0 = 0; c0 < NC; c0 += CB) {
+    if (c0 < p.nchunk) {
+      u32x4 a[CB], b[CB];
+#pragma unroll
+      for (int i = 0; i < CB; ++i) {
+        const int c = min(c0 + i, p.nchunk - 1);
+        a[i] = *(const u32x4*)(wrow + c * KC * ESZ / 4);
+        b[i] = *(const u32x4*)(urow + c * KC * ESZ / 4);
+      }
+#pragma unroll
+      for (int i = 0; i < CB; ++i) {
+        if (col >= P || c0 + i >= p.nchunk) b[i] = u32x4{0u, 0u, 0u, 0u};
+        acc = mfma_chunk<DT>(a[i], b[i], acc);
+        mag = mfma_chunk<DT>(a[i] & kAbs, b[i] & kAbs, mag);
+      }
     }
   }
   // C[token 4 grp + i][row col]
@@ -2127,10 +2200,15 @@ __device__ void row_bounds(const Plan& p, int d, int P, int req, NextShared& nx)
   for (int s = wave; s < P; s += nwave) {
     const float z = lane < np ? nx.zl[s * kProbe + lane] : kNegBig;
     const float a = wave_max_f32(lane < np ? nx.al[s * kProbe + lane] : 0.0f);
+    // the row's kProbe logits in registers (one batch of LDS reads)
+    f32x4 zv[kProbe / 4];
+#pragma unroll
+    for (int i = 0; i < kProbe / 4; ++i) zv[i] = *(const f32x4*)(nx.zl + s * kProbe + 4 * i);
     int rank = 0;
-    for (int q = 0; q < np; ++q) {
-      const float o = nx.zl[s * kProbe + q];
-      rank += o > z || (o == z && q < lane);
+#pragma unroll
+    for (int q = 0; q < kProbe; ++q) {
+      const float o = zv[q / 4][q % 4];
+      rank += q < np && (o > z || (o == z && q < lane));
     }
     if (lane < np && rank == p.kk - 1)
       p.tau[(size_t)req * P + s] = z - 1e-3f * (1.0f + a);
@@ -2172,17 +2250,23 @@ __device__ void select_tail(const Plan& p, int d, int P, int req, SelShared& ssh
   // (the Shared-Markov and parent-independent modes: the one row of the
   // stage serves every frontier parent of the tree)
   const State st{nx.front_node, nx.front_tok, nx.front_score, nx.top_key, nx.top_node, req};
-  stage_select(p, st, d, Pf, req, 1, ssh, false, p.mode != 0);
+  // next head input: the new frontier's tokens, or the greedy chain's token
+  // (Shared-Markov, known before the selection), or zero
+  // (parent-independent); its E loads are issued as soon as the frontier is
+  // known and land during the top-N merge
+  const bool more = d + 1 < p.B;
+  const int Pn = more ? head_rows(p.mode, d + 1, p.kk) : 0;
+  __shared__ int chain_tok[1];
+  if (p.mode != 0 && threadIdx.x == 0) chain_tok[0] = child_key_token(ssh.rowkeys[0][0]);
+  const int* toks = p.mode == 0 ? ssh.next_tok : chain_tok;
+  u32x4 ev0 = {0u, 0u, 0u, 0u};
+  stage_select_body(p, st, d, Pf, req, 1, ssh, false, p.mode != 0, [&] {
+    lds_barrier();
+    if (more) ev0 = next_e_first(p, Pn, toks);
+  });
   tail_writeback(p, req, nx);
-  if (d + 1 < p.B) {
-    // next head input: the new frontier's tokens, or the greedy chain's
-    // token (Shared-Markov), or zero (parent-independent)
-    const int Pn = head_rows(p.mode, d + 1, p.kk);
-    __shared__ int toks[kNarrowRows];
-    if (threadIdx.x < Pn)
-      toks[threadIdx.x] = p.mode == 0 ? ssh.next_tok[threadIdx.x] : child_key_token(ssh.rowkeys[0][0]);
-    __syncthreads();
-    next_inputs(p, d + 1, Pn, req, toks, nx);
+  if (more) {
+    next_inputs(p, d + 1, Pn, req, toks, nx, &ev0);
     if (stage_wide(p.mode, d + 1, p.R, p.kk) && !p.unbounded) row_bounds(p, d + 1, Pn, req, nx);
   }
 }
@@ -2255,6 +2339,8 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Plan p, int d, i
 constexpr int kWideWaves = 8;       // waves of a wide head workgroup
 constexpr int kThrRows = kWideWaves * kTile;  // rows of one column group: 8 blocks of 16
 constexpr int kThrSlots = 4;        // super-tiles (two W tiles) in the LDS ring
+constexpr int kLUnits = 64;         // 16-byte units of L_d per ring slot (one load instruction)
+constexpr int kLWave = 7;           // the wave that loads L_d into the ring
 
 // LDS of head_thr_kernel.  The ring slots are separate objects, so that the
 // compiler can tell the slot being loaded from the one being read (a load
@@ -2312,7 +2398,7 @@ __device__ __forceinline__ void thr_row_slow(const Plan& p, const float (&z)[4],
 // at a time, with full per-lane top-KMAX lists, and each row's KMAX best keys
 // are published.  All threads of the workgroup call it.
 template <int DT, int NCMAX, int KMAX>
-__device__ void thr_exact(const Plan& p, int d, int P, int slice, int t0, int t1, const int* ovl,
+__device__ __forceinline__ void thr_exact(const Plan& p, int d, int P, int slice, int t0, int t1, const int* ovl,
                           int nov, uint64_t* scratch) {
   const int wave = threadIdx.x >> 6;
   for (int b = 0; b < nov; b += kTile) {
@@ -2406,6 +2492,7 @@ __global__ __launch_bounds__(kWideWaves * 64) void head_thr_kernel(Plan p, int d
   constexpr int GROUP = CPW + 2;     // vector-memory instructions per super-tile per wave
   typedef uint32_t lvec __attribute__((ext_vector_type(LW)));
   __shared__ u32x4 ring0[SH::kSlot0], ring1[SH::kSlot], ring2[SH::kSlot], ring3[SH::kSlot];
+  __shared__ u32x4 lslot[kThrSlots][kLUnits];  // L_d of the group's requests per super-tile
   __shared__ uint64_t cand[kThrRows * KMAX];  // each row's candidates
   __shared__ int ccnt[kThrRows];              // their count (past KMAX: overflow)
   __shared__ float2 msx[kThrRows];            // the second wave's row statistics
@@ -2436,6 +2523,16 @@ __global__ __launch_bounds__(kWideWaves * 64) void head_thr_kernel(Plan p, int d
   const bool ok0 = gr0 < rows, ok1 = gr1 < rows;
   const bool live = row0 + 2 * pair * kTile < rows;  // the wave has a row to compute
   const int q0 = ok0 ? gr0 / P : 0, q1 = ok1 ? gr1 / P : 0;  // requests of the two rows
+  // L_d goes through the ring (as W does) when the group's requests fit one
+  // load instruction per super-tile and their rows are 16-byte aligned;
+  // otherwise each lane loads its own L_d words into registers
+  constexpr int TPU = 16 / ESZ;            // tokens per 16-byte unit
+  constexpr int UPR = 2 * kTile / TPU;     // units of one request's row per super-tile
+  const int q_lo = row0 / P;
+  const int nq = (min(row0 + kThrRows, rows) - 1) / P - q_lo + 1;
+  const bool lds_l = nq * UPR <= kLUnits && p.V % TPU == 0 && p.V >= 2 * kTile &&
+                     ((uintptr_t)p.L & 15) == 0;
+  const int j0 = min(max(q0 - q_lo, 0), nq - 1), j1 = min(max(q1 - q_lo, 0), nq - 1);
 
   for (int i = tid; i < kThrRows; i += blockDim.x) ccnt[i] = 0;
   if (tid == 0) ovl[kThrRows] = 0;
@@ -2465,7 +2562,9 @@ __global__ __launch_bounds__(kWideWaves * 64) void head_thr_kernel(Plan p, int d
   // padding puts the 16 rows of an MFMA A-fragment read (one unit each) in 16
   // different bank groups.  Tokens past the slice or V re-read the last one.
   // (slot == s % kThrSlots, passed as a constant of the unrolled loops)
-  auto issue = [&](int s, int slot, lvec (&l)[2]) {
+  // (LL: L_d goes through the ring; otherwise into the lane's registers)
+  auto issue = [&](auto ll, int s, int slot, lvec (&l)[2]) __attribute__((always_inline)) {
+    constexpr bool LL = decltype(ll)::value;
 #pragma unroll
     for (int q = 0; q < CPW; ++q) {
       const int row = wave + q * kWideWaves;  // token row of the super-tile
@@ -2474,115 +2573,185 @@ __global__ __launch_bounds__(kWideWaves * 64) void head_thr_kernel(Plan p, int d
       const char* src = (const char*)p.Wt + (size_t)tok * p.r * ESZ + (size_t)min(lane, ru - 1) * 16;
       if (lane < ru) load_lds16(src, slot_ptr(slot) + row * (ru + 1));
     }
-    const int t = min(t0 + 2 * s + half, t1 - 1);
-    const int tb = min(t * kTile + lg * 4, p.V - 4 > 0 ? p.V - 4 : 0);
-    if (lvec_ok && p.V >= 4) {
-      l[0] = *(const lvec*)(lrow0 + (size_t)tb * ESZ);
-      l[1] = *(const lvec*)(lrow1 + (size_t)tb * ESZ);
-    } else {  // (unaligned rows: word by word, still two vector-memory instructions' worth)
-      lvec a, b;
-#pragma unroll
-      for (int i = 0; i < LW; ++i) { a[i] = 0u; b[i] = 0u; }
-      const int tb2 = t * kTile + lg * 4;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int v = min(tb2 + i, p.V - 1);
-        const uint32_t ra = load_raw<DT>(p.L, ((size_t)q0 * p.B + d) * p.V + v);
-        const uint32_t rb = load_raw<DT>(p.L, ((size_t)q1 * p.B + d) * p.V + v);
-        if (DT) {
-          a[i / 2] |= ra << (16 * (i & 1));
-          b[i / 2] |= rb << (16 * (i & 1));
-        } else {
-          a[i] = ra;
-          b[i] = rb;
-        }
+    if constexpr (LL) {
+      // one wave loads every request's L_d words of the super-tile: lane l
+      // takes unit l % UPR of request l / UPR (lanes past the requests
+      // repeat the last one; units past V re-read the row's last unit)
+      if (wave == kLWave) {
+        const int j = min(lane / UPR, nq - 1), u = lane - (lane / UPR) * UPR;
+        const int tk = min((t0 + 2 * s) * kTile + u * TPU, p.V - TPU);
+        load_lds16((const char*)p.L + (((size_t)(q_lo + j) * p.B + d) * p.V + tk) * ESZ,
+                   &lslot[slot][0]);
       }
-      l[0] = a;
-      l[1] = b;
+    } else {
+      const int t = min(t0 + 2 * s + half, t1 - 1);
+      const int tb = min(t * kTile + lg * 4, p.V - 4 > 0 ? p.V - 4 : 0);
+      if (lvec_ok && p.V >= 4) {
+        l[0] = *(const lvec*)(lrow0 + (size_t)tb * ESZ);
+        l[1] = *(const lvec*)(lrow1 + (size_t)tb * ESZ);
+      } else {  // (unaligned rows: word by word)
+        lvec a, b;
+#pragma unroll
+        for (int i = 0; i < LW; ++i) { a[i] = 0u; b[i] = 0u; }
+        const int tb2 = t * kTile + lg * 4;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int v = min(tb2 + i, p.V - 1);
+          const uint32_t ra = load_raw<DT>(p.L, ((size_t)q0 * p.B + d) * p.V + v);
+          const uint32_t rb = load_raw<DT>(p.L, ((size_t)q1 * p.B + d) * p.V + v);
+          if (DT) {
+            a[i / 2] |= ra << (16 * (i & 1));
+            b[i / 2] |= rb << (16 * (i & 1));
+          } else {
+            a[i] = ra;
+            b[i] = rb;
+          }
+        }
+        l[0] = a;
+        l[1] = b;
+      }
     }
   };
   // the four L_d values of the lane's tokens (tokens tb .. tb + 3 of its
-  // tile, realigned when the vector load had to start earlier)
-  auto lval = [&](const lvec& l, int tb, int i) -> float {
-    const int shift = (lvec_ok && p.V >= 4) ? tb - min(tb, p.V - 4 > 0 ? p.V - 4 : 0) : 0;
+  // tile, realigned when a register vector load had to start earlier)
+  auto lval = [&](auto ll, const lvec& l, int tb, int i) __attribute__((always_inline)) -> float {
+    constexpr bool LL = decltype(ll)::value;
+    const int shift = (!LL && lvec_ok && p.V >= 4) ? tb - min(tb, p.V - 4 > 0 ? p.V - 4 : 0) : 0;
     const int e = min(i + shift, 3);
     return DT ? __uint_as_float((e & 1) ? (l[e / 2] & 0xffff0000u) : (l[e / 2] << 16))
               : __uint_as_float(l[e]);
   };
 
-  // the first super-tiles' loads, then the head inputs of the wave's rows
-  // (B fragments, in flight behind them), then one wait for everything: the
-  // candidate counts are zero for every wave before any appends (the ring's
-  // barriers below do not wait for LDS stores), and the ring's counted waits
-  // start from an empty queue
-  lvec lring[kThrSlots][2];
-#pragma unroll
-  for (int i = 0; i + 1 < kThrSlots; ++i)
-    if (i < nsup) issue(i, i, lring[i]);
+  // the head inputs of the wave's rows (B fragments) and the bounds first,
+  // waited for at once: with no compiler-issued load in flight, the
+  // compiler puts no wait of its own into the ring loop (it cannot count
+  // the ring's loads, so any wait it placed there would drain the whole
+  // ring).  The register path's L_d loads do get such waits; it serves
+  // only groups with many requests or unaligned rows.
   u32x4 b0[NCMAX], b1[NCMAX];
   load_urow<DT, NCMAX>(p, P, gr0, ok0 && live, lg, b0);
   load_urow<DT, NCMAX>(p, P, gr1, ok1 && live, lg, b1);
-  __syncthreads();
+  wait_vmcnt<0>();
 
-  for (int sb = 0; sb < nsup; sb += kThrSlots) {
+  auto stream = [&](auto ll) __attribute__((always_inline)) {
+    constexpr bool LL = decltype(ll)::value;
+    // the first super-tiles' loads; the barrier also makes the candidate
+    // counts zero for every wave before any appends
+    lvec lring[kThrSlots][2];
 #pragma unroll
-    for (int i = 0; i < kThrSlots; ++i) {
-      const int s = sb + i;
-      if (s >= nsup) break;
-      // this wave's loads of super-tile s (and of its L_d words) have landed
-      // once at most the later super-tiles' loads are outstanding
-      if (s + 2 < nsup)
-        wait_vmcnt<2 * GROUP>();
-      else if (s + 1 < nsup)
-        wait_vmcnt<GROUP>();
-      else
-        wait_vmcnt<0>();
-      // and every wave's: ring slot s is complete, slot s - 1 is free
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);
-      __builtin_amdgcn_s_barrier();
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);
-      if (s + kThrSlots - 1 < nsup)
-        issue(s + kThrSlots - 1, (i + kThrSlots - 1) % kThrSlots,
-              lring[(i + kThrSlots - 1) % kThrSlots]);
-      const int t = t0 + 2 * s + half;
-      if (live && t < t1) {
-        f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
-        // lane: token col of tile `half`, units c * 4 + lg (chunks past the
-        // rank re-read the last one: finite values that meet zero B fragments)
-        const u32x4* a = slot_ptr(i) + (half * kTile + col) * (ru + 1) + lg;  // (s % kThrSlots == i)
+    for (int i = 0; i + 1 < kThrSlots; ++i)
+      if (i < nsup) issue(ll, i, i, lring[i]);
+    __syncthreads();
+    // vector-memory instructions per super-tile of this wave
+    const bool extra = LL && wave == kLWave;
+    for (int sb = 0; sb < nsup; sb += kThrSlots) {
 #pragma unroll
-        for (int c = 0; c < NCMAX; ++c) {
-          const u32x4 av = a[min(c, p.nchunk - 1) * 4];
-          c0 = mfma_chunk<DT>(av, b0[c], c0);
-          c1 = mfma_chunk<DT>(av, b1[c], c1);
-        }
-        const int tb = t * kTile + lg * 4;
-        float z0[4], z1[4];
+      for (int i = 0; i < kThrSlots; ++i) {
+        const int s = sb + i;
+        if (s >= nsup) break;
+        // this wave's loads of super-tile s (and of its L_d words) have
+        // landed once at most the later super-tiles' loads are outstanding
+        const int ahead = min(nsup - 1 - s, kThrSlots - 2);
+        constexpr int G0 = LL ? CPW : GROUP;
+        if (ahead == 0)
+          wait_vmcnt<0>();
+        else if (!extra)
+          ahead == 2 ? wait_vmcnt<2 * G0>() : wait_vmcnt<G0>();
+        else
+          ahead == 2 ? wait_vmcnt<2 * G0 + 2>() : wait_vmcnt<G0 + 1>();
+        // and every wave's: ring slot s is complete, slot s - 1 is free
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_s_barrier();
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        if (s + kThrSlots - 1 < nsup)
+          issue(ll, s + kThrSlots - 1, (i + kThrSlots - 1) % kThrSlots,
+                lring[(i + kThrSlots - 1) % kThrSlots]);
+        const int t = t0 + 2 * s + half;
+        if (live && t < t1) {
+          f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+          // lane: token col of tile `half`, units c * 4 + lg (a row's units
+          // past its rank, up to 4 NCMAX, still lie inside the ring slot)
+          const u32x4* a = slot_ptr(i) + (half * kTile + col) * (ru + 1) + lg;  // (s % kThrSlots == i)
+          if constexpr (LL) {
+            // A fragments in groups of AG, the next group's reads in flight
+            // while this group's MFMAs run (one read at a time would pay the
+            // LDS latency per chunk); the scheduling barriers keep that order
+            // Chunks past the rank (c >= nchunk) are read at their constant
+            // offsets, which stay inside the slot, and skipped: the reads
+            // then need no address register per chunk.
+            constexpr int AG = NCMAX >= 16 ? 2 : 4, NG = (NCMAX + AG - 1) / AG;
+            u32x4 ag[2][AG];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          z0[e] = c0[e] + lval(lring[i][0], tb, e);
-          z1[e] = c1[e] + lval(lring[i][1], tb, e);
-        }
-        const float mx0 = fmaxf(fmaxf(z0[0], z0[1]), fmaxf(z0[2], z0[3]));
-        const float mx1 = fmaxf(fmaxf(z1[0], z1[1]), fmaxf(z1[2], z1[3]));
-        // the careful path: a logit at or above the bound or the running
-        // maximum, or tokens past V (only in the vocabulary's last tile)
-        const bool hot = mx0 >= thr0 || mx1 >= thr1 || tb + 3 >= p.V;
-        if (__builtin_expect(__any(hot), 0)) {
-          if (ok0) thr_row_slow<KMAX>(p, z0, tb, m0, s0, tau0, cand + lr0 * KMAX, ccnt + lr0);
-          if (ok1) thr_row_slow<KMAX>(p, z1, tb, m1, s1, tau1, cand + lr1 * KMAX, ccnt + lr1);
-          thr0 = ok0 ? fminf(tau0, m0) : big;
-          thr1 = ok1 ? fminf(tau1, m1) : big;
-        } else {
+            for (int e = 0; e < AG; ++e) ag[0][e] = a[min(e, NCMAX - 1) * 4];
+#pragma unroll
+            for (int g = 0; g < NG; ++g) {
+              if (g + 1 < NG) {
+#pragma unroll
+                for (int e = 0; e < AG; ++e)
+                  ag[(g + 1) & 1][e] = a[min((g + 1) * AG + e, NCMAX - 1) * 4];
+              }
+              __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+              for (int e = 0; e < AG; ++e) {
+                const int c = g * AG + e;
+                if (c < NCMAX && c < p.nchunk) {
+                  c0 = mfma_chunk<DT>(ag[g & 1][e], b0[c], c0);
+                  c1 = mfma_chunk<DT>(ag[g & 1][e], b1[c], c1);
+                }
+              }
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          } else {
+#pragma unroll
+            for (int c = 0; c < NCMAX; ++c) {
+              const u32x4 av = a[c * 4];
+              if (c < p.nchunk) {
+                c0 = mfma_chunk<DT>(av, b0[c], c0);
+                c1 = mfma_chunk<DT>(av, b1[c], c1);
+              }
+            }
+          }
+          const int tb = t * kTile + lg * 4;
+          lvec la, lb;
+          if constexpr (LL) {  // the rows' requests' L_d words of the lane's four tokens
+            const char* lo = (const char*)&lslot[i][0] + (half * kTile + lg * 4) * ESZ;
+            la = *(const lvec*)(lo + j0 * UPR * 16);
+            lb = *(const lvec*)(lo + j1 * UPR * 16);
+          } else {
+            la = lring[i][0];
+            lb = lring[i][1];
+          }
+          float z0[4], z1[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            s0 += exp2_raw((z0[e] - m0) * kLog2e);
-            s1 += exp2_raw((z1[e] - m1) * kLog2e);
+            z0[e] = c0[e] + lval(ll, la, tb, e);
+            z1[e] = c1[e] + lval(ll, lb, tb, e);
+          }
+          const float mx0 = fmaxf(fmaxf(z0[0], z0[1]), fmaxf(z0[2], z0[3]));
+          const float mx1 = fmaxf(fmaxf(z1[0], z1[1]), fmaxf(z1[2], z1[3]));
+          // the careful path: a logit at or above the bound or the running
+          // maximum, or tokens past V (only in the vocabulary's last tile)
+          const bool hot = mx0 >= thr0 || mx1 >= thr1 || tb + 3 >= p.V;
+          if (__builtin_expect(__any(hot), 0)) {
+            if (ok0) thr_row_slow<KMAX>(p, z0, tb, m0, s0, tau0, cand + lr0 * KMAX, ccnt + lr0);
+            if (ok1) thr_row_slow<KMAX>(p, z1, tb, m1, s1, tau1, cand + lr1 * KMAX, ccnt + lr1);
+            thr0 = ok0 ? fminf(tau0, m0) : big;
+            thr1 = ok1 ? fminf(tau1, m1) : big;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              s0 += exp2_raw((z0[e] - m0) * kLog2e);
+              s1 += exp2_raw((z1[e] - m1) * kLog2e);
+            }
           }
         }
       }
     }
-  }
+  };
+  if (lds_l)
+    stream(std::true_type{});
+  else
+    stream(std::false_type{});
   __syncthreads();  // the ring is free for the exact path; candidates complete
 
   // the row statistics: the four lane groups, then the two waves of a row
@@ -2638,6 +2807,7 @@ __global__ __launch_bounds__(kSelectThreads) void mergesel_kernel(Plan p, int d,
   __shared__ SelShared ssh;
   __shared__ NextShared nx;
   __shared__ __attribute__((aligned(16))) uint64_t mk[kNarrowRows][kMergeCap];
+  __shared__ int msrc[kNarrowRows][kMergeCap];  // where each gathered key comes from
   const int req = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   // the lane's slices of its wave's row (at most kSlicesMax / 64):
@@ -2678,11 +2848,25 @@ __global__ __launch_bounds__(kSelectThreads) void mergesel_kernel(Plan p, int d,
     off -= mine;
     uint64_t* keys = mk[wave];
     if (n <= kMergeCap) {
+      // first where each key sits (LDS stores only), then every key's load
+      // in flight at once: a load per key in turn would pay its latency
+      // once per candidate
+      int* src = msrc[wave];
 #pragma unroll
-      for (int i = 0; i < SPL; ++i) {
-        const size_t o = (size_t)gr * kSlicesMax + min(lane + 64 * i, p.G - 1);
-        for (int j = 0; j < c[i]; ++j) keys[off++] = p.part_key[o * KMAX + j];
+      for (int i = 0; i < SPL; ++i)
+        for (int j = 0; j < c[i]; ++j) src[off++] = (lane + 64 * i) * KMAX + j;
+      __builtin_amdgcn_wave_barrier();
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      const uint64_t* rk = p.part_key + (size_t)gr * kSlicesMax * KMAX;
+      uint64_t kv[kMergeCap / 64];
+#pragma unroll
+      for (int t = 0; t < kMergeCap / 64; ++t) {
+        const int e = lane + 64 * t;
+        kv[t] = e < n ? rk[src[e]] : 0;
       }
+#pragma unroll
+      for (int t = 0; t < kMergeCap / 64; ++t)
+        if (lane + 64 * t < n) keys[lane + 64 * t] = kv[t];
     }
     __builtin_amdgcn_wave_barrier();
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
