@@ -1262,6 +1262,11 @@ struct SelShared {
   __attribute__((aligned(16))) uint64_t ckey[256];  // node keys of the stage's candidates
   int rank[256];
   __attribute__((aligned(16))) uint64_t tkey[PCTREE_EMIT_MAX_N];  // a request's top-N keys
+  __attribute__((aligned(16))) uint64_t sk[256];  // the surviving candidates' keys, by request
+  int sci[256];         // and their candidate indices
+  int rstart[17];       // each request's first survivor (and the total after the last)
+  uint32_t tord[16];    // each request's survival threshold (high word of a key)
+  int wcnt[kSelectThreads / 64];  // survivors per wave
   int abort;  // a wait of the selection timed out
 };
 
@@ -1308,15 +1313,70 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
   // (the frontier's loads above have returned: LDS barriers suffice until
   // the frontier is rewritten)
   lds_barrier();
-  // rank within the request's layer, T lanes per candidate
-  {
-    const int T = group_lanes(ncand, blockDim.x);
-    const int c = tid / T;
-    const bool live = c < ncand;
-    const int rq = live ? c / per_req : 0;
-    const int cnt = count_greater_group(sh.ckey + rq * per_req, live ? per_req : 0,
-                                        live ? sh.ckey[c] : 0, tid & (T - 1), T);
+  // With many candidates per request (config-sized layers of 128 and up),
+  // only those that can still enter the next frontier or the running top-N
+  // are ranked.  A parent's children are sorted, so its first child scores
+  // highest; with P >= k' parents, the k' best candidates all score at
+  // least the lowest of those P firsts.  A candidate entering a full top-N
+  // scores at least its last entry.  Candidates scoring below both
+  // thresholds (compared on the key's high word, the ordered score) are
+  // dropped; every survivor's rank among all candidates equals its rank
+  // among the survivors, and every dropped one ranks below every survivor
+  // and every top-N entry.  Smaller layers are ranked whole, one thread per
+  // candidate (the pruning's extra barriers cost more than they save).
+  const int ncur = min(p.N, nbase);
+  const bool prune = per_req >= 128;
+  if (prune) {
+    if (tid < nreq) {
+      uint32_t tf = more ? 0u : 0xFFFFFFFFu;
+      if (more && P >= kk) {
+        tf = 0xFFFFFFFFu;
+        for (int pr = 0; pr < P; ++pr)
+          tf = min(tf, (uint32_t)(sh.ckey[tid * per_req + pr * kk] >> 32));
+      }
+      const uint32_t tn =
+          ncur == p.N
+              ? (uint32_t)(st.top_key[(size_t)(req0 + tid - st.rbase) * p.N + p.N - 1] >> 32)
+              : 0u;
+      sh.tord[tid] = min(tf, tn);
+    }
+    lds_barrier();
+    // the survivors, compacted in candidate order (so each request's are
+    // contiguous): wave counts, then each lane's exclusive prefix
+    const int lane = tid & 63, wave = tid >> 6;
+    const bool surv = tid < ncand && (uint32_t)(sh.ckey[tid] >> 32) >= sh.tord[tid / per_req];
+    const uint64_t bal = __ballot(surv);
+    if (lane == 0) sh.wcnt[wave] = __popcll(bal);
+    lds_barrier();
+    int total = 0, base = 0;
+    for (int w = 0; w < (ncand + 63) / 64; ++w) {
+      const int c = sh.wcnt[w];
+      base += w < wave ? c : 0;
+      total += c;
+    }
+    if (tid < ncand) {
+      const int pos = base + __popcll(bal & ((1ull << lane) - 1));
+      if (surv) {
+        sh.sk[pos] = sh.ckey[tid];
+        sh.sci[pos] = tid;
+      }
+      sh.rank[tid] = 0x7FFFFFFF;  // (a survivor's is set below)
+      if (tid % per_req == 0) sh.rstart[tid / per_req] = pos;
+    }
+    if (tid == 0) sh.rstart[nreq] = total;
+    lds_barrier();
+    // each survivor's rank among its request's survivors, T lanes each
+    const int T = group_lanes(total, blockDim.x);
+    const int e = tid / T;
+    const bool live = e < total;
+    const int c = live ? sh.sci[e] : 0;
+    const int s0 = sh.rstart[c / per_req];
+    const int n = live ? sh.rstart[c / per_req + 1] - s0 : 0;
+    const int cnt = count_greater_group(sh.sk + s0, n, live ? sh.sk[e] : 0, tid & (T - 1), T);
     if (live && (tid & (T - 1)) == 0) sh.rank[c] = cnt;
+  } else if (tid < ncand) {
+    const int rq = tid / per_req;
+    sh.rank[tid] = count_greater(sh.ckey + rq * per_req, per_req, sh.ckey[tid]);
   }
   lds_barrier();
   // next frontier (every frontier slot was read above, before the barriers)
@@ -1356,7 +1416,6 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
   // before any element moves.  The state is in LDS (every caller keeps a
   // copy there), so LDS barriers order it; the global stores above need no
   // wait until the barrier that ends the stage.
-  const int ncur = min(p.N, nbase);
   for (int rq = 0; rq < nreq; ++rq) {
     const int req = req0 + rq;
     uint64_t* tk = st.top_key + (size_t)(req - st.rbase) * p.N;
@@ -1364,17 +1423,21 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
     lds_barrier();
     for (int i = tid; i < ncur; i += blockDim.x) sh.tkey[i] = tk[i];
     lds_barrier();
+    // the request's candidates: its survivors, or all of them
+    const int s0 = prune ? sh.rstart[rq] : rq * per_req;
+    const int ns = prune ? sh.rstart[rq + 1] - s0 : per_req;
+    const uint64_t* keys = prune ? sh.sk : sh.ckey;
     int pos = p.N, node = 0;
     uint64_t key = 0;
-    if (tid < per_req) {
-      const int c = rq * per_req + tid;
-      key = sh.ckey[c];
+    if (tid < ns) {
+      const int c = prune ? sh.sci[s0 + tid] : s0 + tid;
+      key = keys[s0 + tid];
       pos = sh.rank[c] + count_greater(sh.tkey, ncur, key);
-      node = nbase + tid;
+      node = nbase + c - rq * per_req;
     } else if (tid >= 256 && tid < 256 + ncur) {
       const int i = tid - 256;
       key = sh.tkey[i];
-      pos = i + count_greater(sh.ckey + rq * per_req, per_req, key);
+      pos = i + count_greater(keys + s0, ns, key);
       node = tn[i];
     }
     lds_barrier();
@@ -2010,6 +2073,7 @@ __global__ __launch_bounds__(kProbeThreads) void probe_kernel(Plan p) {
 // LDS of the per-request select kernels beyond the selection: the next
 // stage's head input rows (32-bit words) and the probe logits.
 constexpr int kProbeRowWords = 256 + 4;  // a W row of at most 1 KB, padded by 16 bytes
+constexpr int kProbeSplit = 8;  // waves sharing one probe tile's chunks
 
 struct NextShared {
   // the request's selection state: a copy of its workspace entries
@@ -2026,6 +2090,8 @@ struct NextShared {
   __attribute__((aligned(16))) uint32_t u[kNarrowRows * 256];  // rows of at most 1 KB
   __attribute__((aligned(16))) float zl[kNarrowRows * kProbe];
   float al[kNarrowRows * kProbe];
+  // the probe logits' per-wave shares: [tile][share][token][row]
+  float pz[2 * kProbeSplit * kTile * kTile], pa[2 * kProbeSplit * kTile * kTile];
 };
 
 // Loads of a request's select kernel that do not depend on the stage's
@@ -2035,32 +2101,73 @@ struct NextShared {
 // call it; the caller synchronises before using nx.
 __device__ void tail_prefetch(const Plan& p, int d, int req, NextShared& nx) {
   const int tid = threadIdx.x, nth = blockDim.x;
-  for (int i = tid; i < p.kk; i += nth) {
-    nx.front_node[i] = p.front_node[req * p.kk + i];
-    nx.front_tok[i] = p.front_tok[req * p.kk + i];
-    nx.front_score[i] = p.front_score[req * p.kk + i];
+  const bool more = d + 1 < p.B;
+  const bool probes = more && stage_wide(p.mode, d + 1, p.R, p.kk) && !p.unbounded;
+  const int words = p.r * (p.dtype ? 2 : 4) / 4;
+  const int units = kProbe * words / 4;  // 16-byte units of the probe rows
+  const size_t pb = ((size_t)req * p.B + d + 1) * kProbe;
+  const float* hrow = p.h + ((size_t)req * p.B + d + 1) * p.r;
+  const u32x4* src = (const u32x4*)p.probe_w + pb * words / 4;
+  // the thread's first two entries of every kind: all loads first, then the
+  // LDS stores (a load and its store in turn would pay one latency per kind)
+  int fn = 0, ft = 0;
+  float fs = 0.0f, hv[2] = {0.0f, 0.0f}, pl = 0.0f;
+  uint64_t tk[2] = {0, 0};
+  int tn[2] = {0, 0}, pt = 0;
+  u32x4 pw[2];
+  if (tid < p.kk) {
+    fn = p.front_node[req * p.kk + tid];
+    ft = p.front_tok[req * p.kk + tid];
+    fs = p.front_score[req * p.kk + tid];
   }
-  for (int i = tid; i < p.N; i += nth) {
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int i = tid + k * nth;
+    if (i < p.N) {
+      tk[k] = p.top_key[(size_t)req * p.N + i];
+      tn[k] = p.top_node[(size_t)req * p.N + i];
+    }
+    if (more && i < p.r) hv[k] = hrow[i];
+    if (probes && i < units) pw[k] = src[i];
+  }
+  if (probes && tid < kProbe) {
+    pt = p.probe_tok[pb + tid];
+    pl = p.probe_l[pb + tid];
+  }
+  if (tid < p.kk) {
+    nx.front_node[tid] = fn;
+    nx.front_tok[tid] = ft;
+    nx.front_score[tid] = fs;
+  }
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int i = tid + k * nth;
+    if (i < p.N) {
+      nx.top_key[i] = tk[k];
+      nx.top_node[i] = tn[k];
+    }
+    if (more && i < p.r) nx.h[i] = hv[k];
+    if (probes && i < units) {
+      const int q = i / (words / 4);
+      *(u32x4*)&nx.pw[q * kProbeRowWords + 4 * (i - q * (words / 4))] = pw[k];
+    }
+  }
+  if (probes && tid < kProbe) {
+    nx.pt[tid] = pt;
+    nx.pl[tid] = pl;
+  }
+  // the rest (blocks of fewer threads)
+  for (int i = tid + 2 * nth; i < p.N; i += nth) {
     nx.top_key[i] = p.top_key[(size_t)req * p.N + i];
     nx.top_node[i] = p.top_node[(size_t)req * p.N + i];
   }
-  if (d + 1 < p.B) {
-    const float* hrow = p.h + ((size_t)req * p.B + d + 1) * p.r;
-    for (int j = tid; j < p.r; j += nth) nx.h[j] = hrow[j];
-    if (stage_wide(p.mode, d + 1, p.R, p.kk) && !p.unbounded) {
-      const size_t pb = ((size_t)req * p.B + d + 1) * kProbe;
-      if (tid < kProbe) {
-        nx.pt[tid] = p.probe_tok[pb + tid];
-        nx.pl[tid] = p.probe_l[pb + tid];
-      }
-      const int words = p.r * (p.dtype ? 2 : 4) / 4;
-      const uint32_t* src = (const uint32_t*)p.probe_w + pb * words;
-      for (int e = tid; e < kProbe * words; e += nth) {
-        const int q = e / words;
-        nx.pw[q * kProbeRowWords + (e - q * words)] = src[e];
-      }
+  if (more)
+    for (int i = tid + 2 * nth; i < p.r; i += nth) nx.h[i] = hrow[i];
+  if (probes)
+    for (int i = tid + 2 * nth; i < units; i += nth) {
+      const int q = i / (words / 4);
+      *(u32x4*)&nx.pw[q * kProbeRowWords + 4 * (i - q * (words / 4))] = src[i];
     }
-  }
 }
 
 // The request's selection state back to the workspace after its stage.
@@ -2138,44 +2245,46 @@ __device__ void probe_logits(const Plan& p, int P, NextShared& nx) {
   constexpr int KC = DT ? 32 : 16;  // rank elements per MFMA step
   constexpr int ESZ = DT ? 2 : 4;
   constexpr uint32_t kAbs = DT ? 0x7FFF7FFFu : 0x7FFFFFFFu;
-  constexpr int NC = DT ? PCTREE_MAX_RANK_BF16 / 32 : PCTREE_MAX_RANK_F32 / 16;  // chunks at most
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nwave = blockDim.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
   const int np = min(kProbe, p.V);
   const int words = p.r * ESZ / 4;
-  const int q = wave * kTile + col;  // the probe this lane's A row holds
-  const uint32_t* wrow = nx.pw + min(q, kProbe - 1) * kProbeRowWords + grp * (KC / 4) * ESZ / 4;
-  const uint32_t* urow = nx.u + min(col, P - 1) * words + grp * (KC / 4) * ESZ / 4;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f}, mag = {0.f, 0.f, 0.f, 0.f};
-  // four chunks' fragments loaded together per step (chunks past the rank
-  // re-read the last one with a zero B fragment)
-  constexpr int CB = 4;
+  const int ng = min(nwave / 2, kProbeSplit);  // waves per probe tile
+  const int tile = wave & 1, kg = wave >> 1;   // the wave's tile and share of the chunks
+  if (kg < ng) {
+    const int q = tile * kTile + col;  // the probe this lane's A row holds
+    const uint32_t* wrow = nx.pw + q * kProbeRowWords + grp * (KC / 4) * ESZ / 4;
+    const uint32_t* urow = nx.u + min(col, P - 1) * words + grp * (KC / 4) * ESZ / 4;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f}, mag = {0.f, 0.f, 0.f, 0.f};
+    for (int c = kg; c < p.nchunk; c += ng) {
+      const u32x4 a = *(const u32x4*)(wrow + c * KC * ESZ / 4);
+      u32x4 b = *(const u32x4*)(urow + c * KC * ESZ / 4);
+      if (col >= P) b = u32x4{0u, 0u, 0u, 0u};
+      acc = mfma_chunk<DT>(a, b, acc);
+      mag = mfma_chunk<DT>(a & kAbs, b & kAbs, mag);
+    }
+    // the share's C[token 4 grp + i][row col]
+    float* pz = nx.pz + (tile * kProbeSplit + kg) * kTile * kTile;
+    float* pa = nx.pa + (tile * kProbeSplit + kg) * kTile * kTile;
 #pragma unroll
-  for (int c0 = 0; c0 < NC; c0 += CB) {
-    if (c0 < p.nchunk) {
-      u32x4 a[CB], b[CB];
-#pragma unroll
-      for (int i = 0; i < CB; ++i) {
-        const int c = min(c0 + i, p.nchunk - 1);
-        a[i] = *(const u32x4*)(wrow + c * KC * ESZ / 4);
-        b[i] = *(const u32x4*)(urow + c * KC * ESZ / 4);
-      }
-#pragma unroll
-      for (int i = 0; i < CB; ++i) {
-        if (col >= P || c0 + i >= p.nchunk) b[i] = u32x4{0u, 0u, 0u, 0u};
-        acc = mfma_chunk<DT>(a[i], b[i], acc);
-        mag = mfma_chunk<DT>(a[i] & kAbs, b[i] & kAbs, mag);
-      }
+    for (int i = 0; i < 4; ++i) {
+      pz[(4 * grp + i) * kTile + col] = acc[i];
+      pa[(4 * grp + i) * kTile + col] = mag[i];
     }
   }
-  // C[token 4 grp + i][row col]
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int qi = wave * kTile + 4 * grp + i;
-    if (col < P && qi < np) {
+  lds_barrier();
+  // the shares summed (in share order); missing probes get kNegBig
+  for (int e = threadIdx.x; e < 2 * kTile * kTile; e += blockDim.x) {
+    const int t = e / (kTile * kTile), qi = e / kTile, row = e % kTile;  // qi = 16 t + token
+    float z = 0.0f, a = 0.0f;
+    for (int g = 0; g < ng; ++g) {
+      z += nx.pz[(t * kProbeSplit + g) * kTile * kTile + (qi - t * kTile) * kTile + row];
+      a += nx.pa[(t * kProbeSplit + g) * kTile * kTile + (qi - t * kTile) * kTile + row];
+    }
+    if (row < P && qi < np) {
       const bool there = nx.pt[qi] >= 0;
-      nx.zl[col * kProbe + qi] = there ? nx.pl[qi] + acc[i] : kNegBig;
-      nx.al[col * kProbe + qi] = there ? mag[i] + fabsf(nx.pl[qi]) : 0.0f;
+      nx.zl[row * kProbe + qi] = there ? nx.pl[qi] + z : kNegBig;
+      nx.al[row * kProbe + qi] = there ? a + fabsf(nx.pl[qi]) : 0.0f;
     }
   }
 }
@@ -2190,28 +2299,33 @@ __device__ void probe_logits(const Plan& p, int P, NextShared& nx) {
 __device__ void row_bounds(const Plan& p, int d, int P, int req, NextShared& nx) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nwave = blockDim.x >> 6;
   const int np = min(kProbe, p.V);
-  if (wave < (np + kTile - 1) / kTile) {
-    if (p.dtype)
-      probe_logits<1>(p, P, nx);
-    else
-      probe_logits<0>(p, P, nx);
-  }
+  if (p.dtype)
+    probe_logits<1>(p, P, nx);
+  else
+    probe_logits<0>(p, P, nx);
   lds_barrier();
-  for (int s = wave; s < P; s += nwave) {
-    const float z = lane < np ? nx.zl[s * kProbe + lane] : kNegBig;
-    const float a = wave_max_f32(lane < np ? nx.al[s * kProbe + lane] : 0.0f);
-    // the row's kProbe logits in registers (one batch of LDS reads)
+  // two rows per wave: lane 32 h + q holds probe q of row 2 w + h.  A lane
+  // whose logit z has fewer than k' probe logits above it and at least k'
+  // at or above it holds the k'-th best value (tied lanes write the same).
+  const int h = lane >> 5, q = lane & 31;
+  for (int s0 = 2 * wave; s0 < P; s0 += 2 * nwave) {
+    const int s = min(s0 + h, P - 1);
+    const bool live = s0 + h < P && q < np;
+    const float z = q < np ? nx.zl[s * kProbe + q] : kNegBig;
+    float a = q < np ? nx.al[s * kProbe + q] : 0.0f;
+#pragma unroll
+    for (int m = 1; m < 32; m <<= 1) a = fmaxf(a, __shfl_xor(a, m));
     f32x4 zv[kProbe / 4];
 #pragma unroll
     for (int i = 0; i < kProbe / 4; ++i) zv[i] = *(const f32x4*)(nx.zl + s * kProbe + 4 * i);
-    int rank = 0;
+    int gt = 0, ge = 0;
 #pragma unroll
-    for (int q = 0; q < kProbe; ++q) {
-      const float o = zv[q / 4][q % 4];
-      rank += q < np && (o > z || (o == z && q < lane));
+    for (int k = 0; k < kProbe; ++k) {
+      const float o = k < np ? zv[k / 4][k % 4] : -INFINITY;  // (not a probe)
+      gt += o > z;
+      ge += o >= z;
     }
-    if (lane < np && rank == p.kk - 1)
-      p.tau[(size_t)req * P + s] = z - 1e-3f * (1.0f + a);
+    if (live && gt < p.kk && ge >= p.kk) p.tau[(size_t)req * P + s] = z - 1e-3f * (1.0f + a);
   }
   lds_barrier();
 }
