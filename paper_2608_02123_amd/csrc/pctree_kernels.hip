@@ -922,7 +922,12 @@ __device__ void compute_u(const Plan& p, const FrontShared& fs, int d, int P, ch
     for (int q = 0; q < 2; ++q) {
       if (base + q * (int)blockDim.x + (int)threadIdx.x < n) {
         char* dst = ul + (size_t)urow[q] * us;
-        if (DT) {
+        if (p.mode == 2) {  // parent-independent: zero head input
+          if (DT)
+            *(uint2*)(dst + j0[q] * 2) = uint2{0u, 0u};
+          else
+            *(f32x4*)(dst + j0[q] * 4) = f32x4{0.f, 0.f, 0.f, 0.f};
+        } else if (DT) {
           uint16_t u[Q];
 #pragma unroll
           for (int i = 0; i < Q; ++i) u[i] = silu_bf16(__uint_as_float(ev[q][i]), hv[q][i]);
@@ -1048,7 +1053,7 @@ __device__ __forceinline__ void stream_block(const Plan& p, const Plan& sp, Head
   __syncthreads();
 
   for (int d = 0; d < p.B; ++d) {
-    const int P = d == 0 ? 1 : p.kk;
+    const int P = head_rows(p.mode, d, p.kk);
     const HeadLane h(p, P, 0);
     // frontier-independent loads before the wait
     uint32_t lreg[RT][4], llds[LTW][4];
@@ -1132,7 +1137,7 @@ __device__ void stream_block_fold(const Plan& p, const Plan& sp,
   __syncthreads();
 
   for (int d = 0; d < p.B; ++d) {
-    const int P = d == 0 ? 1 : p.kk;
+    const int P = head_rows(p.mode, d, p.kk);
     const HeadLane h(p, P, 0, true);
     // L_d of the lane's own tile of every resident pair, before the wait
     uint32_t lreg[RP][4], llds[LP][4];
@@ -1385,11 +1390,15 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
     const int ci = tid - rq * per_req;
     const int req = req0 + rq;
     const int slot = sh.rank[tid];
-    if (bcast)  // the streaming workgroups wait for these words
+    if (bcast) {  // the streaming workgroups wait for these words
+      // (with one shared row, the next row's token is the greedy chain's:
+      // the row's best child, which slot 0 carries)
+      const int wtok = shared ? min(max(child_key_token(sh.rowkeys[rq][0]), 0), p.V - 1) : tok;
       __hip_atomic_store(p.front_w + (size_t)(d + 1) * p.rows_max + req * kk + slot,
                          ((uint64_t)__float_as_uint(score) << 32) |
-                             ((uint64_t)tok << kTagBits) | p.tag,
+                             ((uint64_t)wtok << kTagBits) | p.tag,
                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     st.front_node[(req - st.rbase) * kk + slot] = nbase + ci;
     st.front_tok[(req - st.rbase) * kk + slot] = tok;
     st.front_score[(req - st.rbase) * kk + slot] = score;
@@ -1865,7 +1874,7 @@ __device__ __forceinline__ Plan scalar_plan(const Plan& lp) {
 template <int DT>
 __device__ __noinline__ void frontier_call(const Plan& lp, int d) {
   const Plan p = scalar_plan(lp);
-  compute_u<DT>(p, g_front, d, d == 0 ? 1 : p.kk, (char*)g_dyn);
+  compute_u<DT>(p, g_front, d, head_rows(p.mode, d, p.kk), (char*)g_dyn);
 }
 
 // Blocks [0, G) stream one V-slice each; block G is the keeper.  A streaming
@@ -1924,15 +1933,17 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
   if (threadIdx.x == 0) ssh.abort = 0;
   __syncthreads();
   for (int d = 0; d < p.B; ++d) {
-    const int P = d == 0 ? 1 : p.kk;
-    if (!sel_merge<KMAX>(p, d, p.R * P, ssh)) {
+    // head rows of the stage (one per request in the control modes) and
+    // frontier parents (Sec. 5.3: the control modes' one row serves them all)
+    const int Ph = head_rows(p.mode, d, p.kk), Pf = d == 0 ? 1 : p.kk;
+    if (!sel_merge<KMAX>(p, d, p.R * Ph, ssh)) {
       abort_outputs(p);
       return;
     }
     if constexpr (kInline)
-      stage_select_body(p, st, d, P, 0, p.R, ssh, true, false);
+      stage_select_body(p, st, d, Pf, 0, p.R, ssh, true, p.mode != 0);
     else
-      stage_select(p, st, d, P, 0, p.R, ssh, true);
+      stage_select(p, st, d, Pf, 0, p.R, ssh, true, p.mode != 0);
   }
   __syncthreads();  // the pool entries stored by the stages are visible to every wave
   for (int req = 0; req < p.R; ++req) {
@@ -3178,7 +3189,7 @@ DebugConfig& debug_config() {
 
 hipError_t launch_round(const Plan& p0, hipStream_t st) {
   const DebugConfig dbg = debug_config();
-  const bool narrow = p0.R * p0.kk <= kNarrowRows && p0.mode == 0 && !dbg.force_multilaunch;
+  const bool narrow = p0.R * p0.kk <= kNarrowRows && !dbg.force_multilaunch;
   Plan p = p0;
   DeviceInfo di;
   RoundFn rfn = nullptr;

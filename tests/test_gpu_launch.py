@@ -73,6 +73,30 @@ def test_tree_independent_of_vocab_slicing(name):
                                    atol=C.SCORE_GUARD)
 
 
+@pytest.mark.parametrize("mode", ["shared", "independent"])
+def test_control_modes_independent_of_launch_form(mode):
+    """The control scorings run in the single-launch round too (one shared
+    row per request and stage): it must emit the tree of the per-stage
+    launches, and both must match the oracle."""
+    w = CONFIGS["qwen4b_b7"]
+    inp = make_inputs(w)
+    dev = P.device_inputs(inp)
+    m = {"shared": P.MODE_SHARED, "independent": P.MODE_INDEPENDENT}[mode]
+    b = _builder(w, mode=m)
+    outs = {}
+    for label, launch in {"single launch": {}, "per-stage launches": {"force_multilaunch": True}}.items():
+        say(f"[launch] {mode}: {label}")
+        outs[label] = _run(b, dev, **launch)
+        reps = C.compare_batch(outs[label], inp, w.k, w.N, mode=mode, label=f"{mode}/{label}")
+        # (parent-independent scores tie exactly: a + b = b + a across parents)
+        assert all(r["exact"] or r["identical"] for r in reps), f"{label}: tree differs from the oracle"
+    for key in TREE_KEYS:
+        assert torch.equal(outs["single launch"][key], outs["per-stage launches"][key]), key
+    np.testing.assert_allclose(outs["single launch"]["logprob"].cpu().numpy(),
+                               outs["per-stage launches"]["logprob"].cpu().numpy(),
+                               atol=C.SCORE_GUARD)
+
+
 def test_abandoned_round_pads_every_output_then_recovers():
     w = CONFIGS["qwen4b_b7"]  # R * k' = 8 rows: the single-launch round
     inp = make_inputs(w)
