@@ -38,13 +38,22 @@ def compile_flags() -> list[str]:
     ]
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every HIP source for gfx950 and link ``libpctree.so``; returns its path."""
+# AddressSanitizer on the host code only (the device code is built as usual):
+# the checking build of the C ABI, loaded with the sanitizer runtime preloaded
+ASAN_LIB = os.path.join(PKG, "libpctree_asan.so")
+ASAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def build(verbose: bool = False, asan: bool = False) -> str:
+    """Compile every HIP source for gfx950 and link ``libpctree.so`` (or, with
+    ``asan``, ``libpctree_asan.so`` with host-side AddressSanitizer); returns its
+    path."""
     cc = hipcc()
+    extra = ASAN_FLAGS if asan else []
     objs, procs = [], []
     for src in SOURCES:  # the sources compile side by side
-        obj = os.path.join(CSRC, src.replace(".hip", ".o"))
-        cmd = [cc, *compile_flags(), "-c", os.path.join(CSRC, src), "-o", obj]
+        obj = os.path.join(CSRC, src.replace(".hip", "_asan.o" if asan else ".o"))
+        cmd = [cc, *compile_flags(), *extra, "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((cmd, subprocess.Popen(cmd, stderr=None if verbose else subprocess.DEVNULL)))
@@ -52,16 +61,17 @@ def build(verbose: bool = False) -> str:
     for cmd, proc in procs:
         if proc.wait() != 0:
             raise subprocess.CalledProcessError(proc.returncode, cmd)
-    tmp = LIB + ".tmp"
-    cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+    out = ASAN_LIB if asan else LIB
+    tmp = out + ".tmp"
+    cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *extra, *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
     for o in objs:
         os.remove(o)
-    return LIB
+    return out
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, asan="--asan" in sys.argv))

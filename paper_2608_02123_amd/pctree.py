@@ -39,7 +39,8 @@ __all__ = [
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libpctree.so")
+# (PCTREE_LIB: another build of the same library, e.g. the host-sanitizer one)
+LIB_PATH = os.environ.get("PCTREE_LIB") or os.path.join(_HERE, "libpctree.so")
 
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 F32, BF16 = 0, 1
