@@ -113,7 +113,9 @@ __device__ __forceinline__ uint16_t bf16_rne(float f) {
 
 // The same bf16 head input, bf16(f32(SiLU(e + h) in float64)), mostly from
 // an f32 evaluation: x = e + h with its exact rounding error (two-sum),
-// exp(-x) by a two-constant ln 2 reduction and the hardware 2^x, the quotient
+// exp(-x) by Cody and Waite's additive range reduction (x - n ln 2 with ln 2
+// split into a short high part, exact in the product, and a low part) and
+// the hardware 2^x on the reduced argument, the quotient
 // x / (1 + exp(-x)) refined by one Newton step, and a first-order correction
 // for the rounding of x.  The result lies within 6 bit steps of
 // f32(SiLU64(x)) by the error analysis (at most 3 seen over 10^9 draws with
