@@ -2755,10 +2755,36 @@ __global__ __launch_bounds__(kWideWaves * 64) void head_thr_kernel(Plan p, int d
   // the ring's loads, so any wait it placed there would drain the whole
   // ring).  The register path's L_d loads do get such waits; it serves
   // only groups with many requests or unaligned rows.
+  // The 128 rows' head inputs go through the idle ring first, each row
+  // loaded once (row i of the group into ring slot i / 32, at the W rows'
+  // padded stride, so that wave pair q's 32 rows fill slot q): the two
+  // waves of a pair then read the same rows from LDS instead of both
+  // fetching them.  Rows past the stage's re-read a valid one and read back
+  // as zero.
   u32x4 b0[NCMAX], b1[NCMAX];
-  load_urow<DT, NCMAX>(p, P, gr0, ok0 && live, lg, b0);
-  load_urow<DT, NCMAX>(p, P, gr1, ok1 && live, lg, b1);
-  wait_vmcnt<0>();
+  {
+    constexpr int RPW = kThrRows / kWideWaves;  // rows per wave
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+      const int i = wave + k * kWideWaves;  // row of the group
+      const int gr = min(row0 + i, rows - 1);
+      const int req = gr / P, slot = gr - req * P;
+      const char* src = (const char*)p.U + ((size_t)(req * p.kk + slot) * p.r) * ESZ +
+                        (size_t)min(lane, ru - 1) * 16;
+      if (lane < ru) load_lds16(src, slot_ptr(i / (2 * kTile)) + (i % (2 * kTile)) * (ru + 1));
+    }
+    wait_vmcnt<0>();
+    __syncthreads();
+    const u32x4* us = slot_ptr(pair) + col * (ru + 1) + lg;
+#pragma unroll
+    for (int c = 0; c < NCMAX; ++c) {
+      const u32x4 v0 = us[c * 4], v1 = us[kTile * (ru + 1) + c * 4];
+      const bool in = c < p.nchunk && live;
+      b0[c] = in && ok0 ? v0 : u32x4{0u, 0u, 0u, 0u};
+      b1[c] = in && ok1 ? v1 : u32x4{0u, 0u, 0u, 0u};
+    }
+    __syncthreads();  // (the prefetch below overwrites the ring)
+  }
 
   auto stream = [&](auto ll) __attribute__((always_inline)) {
     constexpr bool LL = decltype(ll)::value;
