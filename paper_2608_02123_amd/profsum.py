@@ -3,7 +3,7 @@
 ``python -m paper_2608_02123_amd.profsum stats DIR`` prints the per-kernel
 table of a ``--kernel-trace --stats`` run as markdown.
 
-``python -m paper_2608_02123_amd.profsum traffic FETCH_DIR WRITE_DIR OUT.json [WORKLOAD]``
+``python -m paper_2608_02123_amd.profsum traffic FETCH_DIR WRITE_DIR OUT.json [WORKLOAD [KERNEL [STEPS]]]``
 turns two ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` runs of
 ``bench.py --calibrate-copy`` into HBM bytes per round-kernel launch.  Each
 counter is scaled by what it reads for the calibration pass (an elementwise
@@ -60,7 +60,7 @@ def _pick(means: dict[str, tuple[float, int]], needle: str) -> tuple[str, float,
 
 
 def traffic(fetch_dir: str, write_dir: str, kernel: str = "round_kernel",
-            workload: str = "qwen4b_b16") -> dict:
+            workload: str = "qwen4b_b16", steps: int = 20) -> dict:
     f = counter_means(fetch_dir, "FETCH_SIZE")
     w = counter_means(write_dir, "WRITE_SIZE")
     _, f_copy, _ = _pick(f, COPY_KERNEL)
@@ -71,8 +71,8 @@ def traffic(fetch_dir: str, write_dir: str, kernel: str = "round_kernel",
     fw = COPY_BYTES / (w_copy * 1024.0)
     with open(KERNEL_SRC, "rb") as fh:
         sha = hashlib.sha256(fh.read()).hexdigest()[:16]
-    bench = (f"python3 bench.py --workload {workload} --steps 20 --warmup 2 --no-cpu-baseline "
-             "--cold-steps 0 --calibrate-copy")
+    bench = (f"python3 bench.py --workload {workload} --configs \"\" --steps {steps} "
+             f"--warmup {2 if steps >= 20 else 1} --no-cpu-baseline --cold-steps 0 --calibrate-copy")
     return {
         "workload": workload,
         "commands": [
@@ -95,7 +95,9 @@ def main(argv: list[str]) -> None:
     if len(argv) >= 2 and argv[0] == "stats":
         print(stats_markdown(argv[1]))
     elif len(argv) >= 4 and argv[0] == "traffic":
-        t = traffic(argv[1], argv[2], workload=argv[4] if len(argv) > 4 else "qwen4b_b16")
+        t = traffic(argv[1], argv[2], workload=argv[4] if len(argv) > 4 else "qwen4b_b16",
+                    kernel=argv[5] if len(argv) > 5 else "round_kernel",
+                    steps=int(argv[6]) if len(argv) > 6 else 20)
         with open(argv[3], "w") as fh:
             json.dump(t, fh, indent=1)
         print(json.dumps(t, indent=1))
