@@ -59,6 +59,43 @@ typedef struct pctree_debug_config {
  * round_slices is negative. */
 pctree_status pctree_debug_set(const pctree_debug_config* cfg);
 
+/* Stage timeline, for measurement tools that break a round into its steps.
+ * A diagnostic build of the library (libpctree_timeline.so, compiled with
+ * -DPCTREE_TIMELINE) stamps the device wall clock from thread 0 of a few
+ * workgroups at the steps of every stage into a device array
+ * [PCTREE_TIMELINE_WHO][PCTREE_TIMELINE_STAGES][PCTREE_TIMELINE_EVENTS] of
+ * int64 ticks (0: not stamped; the clock runs at a fixed rate and is common
+ * to the whole device).  Each stamp is one global store; the tree is the
+ * same as the default build's.  The default library (libpctree.so) has no
+ * stamps.  Rows of the array (who), stage d:
+ *   0  keeper of the single-launch round: 0 merge starts, 1 every slice
+ *      record seen and the rows merged, 2 stage selected (frontier
+ *      published); stage PCTREE_TIMELINE_STAGES - 1: 0 stages done,
+ *      1 emission done
+ *   1  first streaming workgroup of the single-launch round, 2 the last
+ *      one: 0 frontier wait begins, 1 head input built, 2 stream done,
+ *      3 slice records published
+ *   3  per-stage launches, a stage with more than 16 head rows: workgroup 0
+ *      of the head kernel: 0 start, 1 stream done, 2 end
+ *   4  the same stage's merge-and-select workgroup of request 0: 0 start,
+ *      1 rows merged, 2 end (selection, next head input and row bounds)
+ * Every stage has its row (B <= PCTREE_MAX_BLOCK < PCTREE_TIMELINE_STAGES - 1). */
+#define PCTREE_TIMELINE_WHO 5
+#define PCTREE_TIMELINE_STAGES 65
+#define PCTREE_TIMELINE_EVENTS 8
+
+/* 1 in the timeline build, 0 in the default build. */
+int32_t pctree_timeline_available(void);
+
+/* Copy the stamps (PCTREE_TIMELINE_WHO * PCTREE_TIMELINE_STAGES *
+ * PCTREE_TIMELINE_EVENTS entries, row-major) into `out` and the clock's rate
+ * in ticks per microsecond into `ticks_per_us`, then zero the stamps.  A
+ * blocking copy from the current device: call it once the rounds to read
+ * have finished (and once before them, to start from zero).
+ * PCTREE_ERR_UNSUPPORTED in the default build, PCTREE_ERR_INVALID_ARGUMENT
+ * for a null pointer, PCTREE_ERR_HIP if a copy or the rate query fails. */
+pctree_status pctree_timeline_read(int64_t* out, double* ticks_per_us);
+
 #ifdef __cplusplus
 }
 #endif

@@ -40,6 +40,29 @@
 #define PCTREE_MASK_MAX_N 1024
 
 namespace pctree {
+
+// The stage timeline (a diagnostic build, -DPCTREE_TIMELINE): thread 0 of a
+// few workgroups stamps the device wall clock at the steps of every stage.
+// The default build compiles every stamp away.
+#ifdef PCTREE_TIMELINE
+__device__ long long g_timeline[kTimelineWho][kTimelineStages][kTimelineEvents];
+#define TIMELINE_STAMP(who, stage, ev)                                     \
+  do {                                                                     \
+    if (threadIdx.x == 0 && (stage) >= 0 && (stage) < kTimelineStages)      \
+      g_timeline[(who)][(stage)][(ev)] = (long long)wall_clock64();         \
+  } while (0)
+#else
+#define TIMELINE_STAMP(who, stage, ev) \
+  do {                                 \
+  } while (0)
+#endif
+// the first and the last streaming workgroup of the single-launch round
+#define TIMELINE_SLICE(stage, ev)                                      \
+  do {                                                                 \
+    if (blockIdx.x == 0) TIMELINE_STAMP(1, stage, ev);                 \
+    else if ((int)blockIdx.x == p.G - 1) TIMELINE_STAMP(2, stage, ev); \
+  } while (0)
+
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -1064,7 +1087,9 @@ __device__ __forceinline__ void stream_block(const Plan& p, const Plan& sp, Head
 #pragma unroll
     for (int q = 0; q < LTW; ++q)
       load_lfrag<DT>(p, h, d, min(lds0 + wave + WAVES * q, t1 - 1), llds[q]);
+    TIMELINE_SLICE(d, 0);
     if (!stage_inputs<DT, KMAX>(p, sp, d, fs, sh_go)) return;
+    TIMELINE_SLICE(d, 1);
     u32x4 bfrag[NCMAX];
     load_bfrag_lds<DT, NCMAX>(p, h, ul, bfrag);
     RowAcc<KMAX> r;
@@ -1094,7 +1119,9 @@ __device__ __forceinline__ void stream_block(const Plan& p, const Plan& sp, Head
       load_lfrag<DT>(p, h, d, t, T.l);
       tile_step<DT, NCMAX, KMAX>(p, h, T.a, bfrag, T.l, t, r);
     }
+    TIMELINE_SLICE(d, 2);
     publish_partial<KMAX, WAVES>(p, h, d, slice, r, sh);
+    TIMELINE_SLICE(d, 3);
   }
 }
 
@@ -1149,7 +1176,9 @@ __device__ void stream_block_fold(const Plan& p, const Plan& sp,
 #pragma unroll
     for (int q = 0; q < LP; ++q)
       load_lfrag<DT>(p, h, d, min(lds0 + wave + WAVES * (2 * q + h.half), t1 - 1), llds[q]);
+    TIMELINE_SLICE(d, 0);
     if (!stage_inputs<DT, KMAX>(p, sp, d, fs, sh_go)) return;
+    TIMELINE_SLICE(d, 1);
     u32x4 bfrag[NCMAX];
     load_bfrag_lds<DT, NCMAX>(p, h, ul, bfrag);
     RowAcc<KMAX> r;
@@ -1194,7 +1223,9 @@ __device__ void stream_block_fold(const Plan& p, const Plan& sp,
       load_lfrag<DT>(p, h, d, tl, l);
       tile_pair_step<DT, NCMAX, KMAX>(p, h, a0, a1, bfrag, l, tl, h.half ? okb : true, r);
     }
+    TIMELINE_SLICE(d, 2);
     publish_partial<KMAX, WAVES, true>(p, h, d, slice, r, sh);
+    TIMELINE_SLICE(d, 3);
   }
 }
 
@@ -1938,22 +1969,27 @@ __global__ __launch_bounds__(kRoundWaves * 64) void round_kernel(Plan p) {
     // head rows of the stage (one per request in the control modes) and
     // frontier parents (Sec. 5.3: the control modes' one row serves them all)
     const int Ph = head_rows(p.mode, d, p.kk), Pf = d == 0 ? 1 : p.kk;
+    TIMELINE_STAMP(0, d, 0);
     if (!sel_merge<KMAX>(p, d, p.R * Ph, ssh)) {
       abort_outputs(p);
       return;
     }
+    TIMELINE_STAMP(0, d, 1);
     if constexpr (kInline)
       stage_select_body(p, st, d, Pf, 0, p.R, ssh, true, p.mode != 0);
     else
       stage_select(p, st, d, Pf, 0, p.R, ssh, true, p.mode != 0);
+    TIMELINE_STAMP(0, d, 2);
   }
   __syncthreads();  // the pool entries stored by the stages are visible to every wave
+  TIMELINE_STAMP(0, kTimelineStages - 1, 0);
   for (int req = 0; req < p.R; ++req) {
     if constexpr (kInline)
       emit_request_body(p, st, req);
     else
       emit_request(p, st, req);
   }
+  TIMELINE_STAMP(0, kTimelineStages - 1, 1);
 }
 
 // ---------------------------------------------------------------------------
@@ -2661,6 +2697,7 @@ __global__ __launch_bounds__(kWideWaves * 64) void head_thr_kernel(Plan p, int d
                      ((uintptr_t)p.L & 15) == 0;
   const int j0 = min(max(q0 - q_lo, 0), nq - 1), j1 = min(max(q1 - q_lo, 0), nq - 1);
 
+  if (blockIdx.x == 0) TIMELINE_STAMP(3, d, 0);
   for (int i = tid; i < kThrRows; i += blockDim.x) ccnt[i] = 0;
   if (tid == 0) ovl[kThrRows] = 0;
 
@@ -2906,6 +2943,7 @@ __global__ __launch_bounds__(kWideWaves * 64) void head_thr_kernel(Plan p, int d
   else
     stream(std::false_type{});
   __syncthreads();  // the ring is free for the exact path; candidates complete
+  if (blockIdx.x == 0) TIMELINE_STAMP(3, d, 1);
 
   // the row statistics: the four lane groups, then the two waves of a row
   lse_combine_pair<16>(m0, s0);
@@ -2946,7 +2984,7 @@ __global__ __launch_bounds__(kWideWaves * 64) void head_thr_kernel(Plan p, int d
   __syncthreads();
   const int nov = ovl[kThrRows];
   if (nov > 0)
-    thr_exact<DT, NCMAX, KMAX>(p, d, P, slice, t0, t1, ovl, nov, (uint64_t*)ring0);
+    thr_exact<DT, NCMAX, KMAX>(p, d, P, slice, t0, t1, ovl, nov, (uint64_t*)ring0);  if (blockIdx.x == 0) TIMELINE_STAMP(3, d, 2);
 }
 
 // One WG per request after a wide head stage: each of its rows (one wave per
@@ -2963,6 +3001,7 @@ __global__ __launch_bounds__(kSelectThreads) void mergesel_kernel(Plan p, int d,
   __shared__ int msrc[kNarrowRows][kMergeCap];  // where each gathered key comes from
   const int req = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (req == 0) TIMELINE_STAMP(4, d, 0);
   // the lane's slices of its wave's row (at most kSlicesMax / 64):
   // statistics and counts first, all loads in flight together, then the
   // state and next-stage loads behind them, then the few candidates
@@ -3055,7 +3094,9 @@ __global__ __launch_bounds__(kSelectThreads) void mergesel_kernel(Plan p, int d,
     if (lane == 0) ssh.lse[wave] = M + logf(S);
   }
   __syncthreads();
+  if (req == 0) TIMELINE_STAMP(4, d, 1);
   select_tail(p, d, P, req, ssh, nx);
+  if (req == 0) TIMELINE_STAMP(4, d, 2);
 }
 
 // Zero the words the persistent round polls (slice partials of every stage,
@@ -3329,6 +3370,32 @@ hipError_t launch_mask(const int* parent, const int* count, int R, int N, uint32
                        hipStream_t st) {
   hipLaunchKernelGGL(mask_kernel, dim3(R), dim3(kMaskThreads), 0, st, parent, count, N, mask);
   return hipGetLastError();
+}
+
+bool timeline_built() {
+#ifdef PCTREE_TIMELINE
+  return true;
+#else
+  return false;
+#endif
+}
+
+hipError_t timeline_copy(long long* host, bool clear) {
+#ifdef PCTREE_TIMELINE
+  if (host) {
+    const hipError_t e = hipMemcpyFromSymbol(host, HIP_SYMBOL(g_timeline), sizeof(g_timeline));
+    if (e != hipSuccess) return e;
+  }
+  if (clear) {
+    static const long long zero[kTimelineWho][kTimelineStages][kTimelineEvents] = {};
+    return hipMemcpyToSymbol(HIP_SYMBOL(g_timeline), zero, sizeof(zero));
+  }
+  return hipSuccess;
+#else
+  (void)host;
+  (void)clear;
+  return hipErrorNotSupported;
+#endif
 }
 
 }  // namespace pctree

@@ -120,6 +120,15 @@ DebugConfig& debug_config();
 bool profile_on();
 void profile_mark(hipStream_t stream, const char* kernel);
 
+// Stage timeline of the diagnostic build (compiled with PCTREE_TIMELINE):
+// [who][stage][event] device wall-clock stamps (include/pctree_profile.h
+// lists the workgroups and events).  timeline_copy copies them to `host`
+// (when not null) and then zeroes them if `clear`; hipErrorNotSupported in
+// the default build, which has no stamps.
+constexpr int kTimelineWho = 5, kTimelineStages = 65, kTimelineEvents = 8;
+bool timeline_built();
+hipError_t timeline_copy(long long* host, bool clear);
+
 // Enqueue the standalone ancestor-mask kernel.
 hipError_t launch_mask(const int* parent, const int* count, int R, int N, uint32_t* mask,
                        hipStream_t stream);

@@ -94,4 +94,23 @@ pctree_status pctree_debug_set(const pctree_debug_config* cfg) {
   return PCTREE_OK;
 }
 
+int32_t pctree_timeline_available(void) { return timeline_built() ? 1 : 0; }
+
+pctree_status pctree_timeline_read(int64_t* out, double* ticks_per_us) {
+  static_assert(kTimelineWho == PCTREE_TIMELINE_WHO && kTimelineStages == PCTREE_TIMELINE_STAGES &&
+                    kTimelineEvents == PCTREE_TIMELINE_EVENTS,
+                "timeline shape");
+  static_assert(sizeof(long long) == sizeof(int64_t), "timeline stamps are 64-bit");
+  if (!timeline_built()) return PCTREE_ERR_UNSUPPORTED;
+  if (!out || !ticks_per_us) return PCTREE_ERR_INVALID_ARGUMENT;
+  int dev = 0, khz = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+      khz <= 0)
+    return PCTREE_ERR_HIP;
+  if (timeline_copy(reinterpret_cast<long long*>(out), true) != hipSuccess) return PCTREE_ERR_HIP;
+  *ticks_per_us = khz / 1000.0;
+  return PCTREE_OK;
+}
+
 }  // extern "C"

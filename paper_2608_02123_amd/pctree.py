@@ -28,6 +28,8 @@ __all__ = [
     "tree_attention",
     "TreeAttention",
     "TreeBuilder",
+    "timeline_available",
+    "timeline_read",
     "status_string",
     "DebugConfig",
     "debug_set",
@@ -41,6 +43,9 @@ __all__ = [
 _HERE = os.path.dirname(os.path.abspath(__file__))
 # (PCTREE_LIB: another build of the same library, e.g. the host-sanitizer one)
 LIB_PATH = os.environ.get("PCTREE_LIB") or os.path.join(_HERE, "libpctree.so")
+# the stage-timeline build of the same library (include/pctree_profile.h)
+TIMELINE_LIB_PATH = os.path.join(_HERE, "libpctree_timeline.so")
+TIMELINE_WHO, TIMELINE_STAGES, TIMELINE_EVENTS = 5, 65, 8
 
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 F32, BF16 = 0, 1
@@ -145,6 +150,10 @@ def lib() -> ctypes.CDLL:
         L.pctree_profile_read.restype = ctypes.c_int
         L.pctree_debug_set.argtypes = [ctypes.POINTER(DebugConfig)]
         L.pctree_debug_set.restype = ctypes.c_int
+        L.pctree_timeline_available.argtypes = []
+        L.pctree_timeline_available.restype = ctypes.c_int32
+        L.pctree_timeline_read.argtypes = [vp, ctypes.POINTER(ctypes.c_double)]
+        L.pctree_timeline_read.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -336,6 +345,28 @@ def profile_read():
     _check(lib().pctree_profile_read(ctypes.byref(ms), ctypes.byref(n), ctypes.byref(name)),
            "pctree_profile_read")
     return ms.value, n.value, name.value.decode()
+
+
+def timeline_available() -> bool:
+    """Whether the loaded library is the stage-timeline build."""
+    return bool(lib().pctree_timeline_available())
+
+
+def timeline_read():
+    """The stage timeline's stamps in microseconds, as a float64 array
+    [who][stage][event] (NaN where not stamped), zeroing them
+    (pctree_timeline_read; waits for the current device first)."""
+    import numpy as np
+
+    torch.cuda.synchronize()
+    n = TIMELINE_WHO * TIMELINE_STAGES * TIMELINE_EVENTS
+    buf = (ctypes.c_int64 * n)()
+    rate = ctypes.c_double()
+    _check(lib().pctree_timeline_read(ctypes.cast(buf, ctypes.c_void_p), ctypes.byref(rate)),
+           "pctree_timeline_read")
+    ticks = np.frombuffer(buf, dtype=np.int64).reshape(TIMELINE_WHO, TIMELINE_STAGES,
+                                                       TIMELINE_EVENTS)
+    return np.where(ticks > 0, ticks / rate.value, np.nan)
 
 
 def build_mask(parent, count, stream=None):

@@ -11,22 +11,30 @@ import pytest
 
 from paper_2608_02123_amd import pctree as P
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "pctree.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include")
+HEADERS = sorted(os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h"))
 A = 0x100000  # fake, suitably aligned device addresses (validation never dereferences)
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    return sorted(set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(pctree_\w+)\s*\(", text, re.M)))
+    names = set()
+    for h in HEADERS:
+        text = open(h).read()
+        names |= set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(pctree_\w+)\s*\(", text, re.M))
+    return sorted(names)
 
 
 def test_exports_every_declared_symbol():
+    """Every function that include/*.h declares, in the default library and
+    in its stage-timeline build."""
     names = declared_functions()
     assert {"pctree_build_tree", "pctree_build_mask", "pctree_chain_decode",
-            "pctree_workspace_bytes", "pctree_status_string", "pctree_abi_version"} <= set(names)
-    lib = ctypes.CDLL(P.LIB_PATH)
-    for n in names:
-        assert hasattr(lib, n), n
+            "pctree_workspace_bytes", "pctree_status_string", "pctree_abi_version",
+            "pctree_profile_enable", "pctree_debug_set", "pctree_timeline_read"} <= set(names)
+    for path in (P.LIB_PATH, P.TIMELINE_LIB_PATH):
+        lib = ctypes.CDLL(path)
+        for n in names:
+            assert hasattr(lib, n), (path, n)
     assert P.lib().pctree_abi_version() == 1
 
 
