@@ -2122,7 +2122,7 @@ __global__ __launch_bounds__(kProbeThreads) void probe_kernel(Plan p) {
 // LDS of the per-request select kernels beyond the selection: the next
 // stage's head input rows (32-bit words) and the probe logits.
 constexpr int kProbeRowWords = 256 + 4;  // a W row of at most 1 KB, padded by 16 bytes
-constexpr int kProbeSplit = 8;  // waves sharing one probe tile's chunks
+constexpr int kProbeSplit = 2;  // waves sharing one probe tile's chunks
 
 struct NextShared {
   // the request's selection state: a copy of its workspace entries
@@ -2284,11 +2284,14 @@ __device__ void next_inputs(const Plan& p, int d, int P, int req, const int* tok
   lds_barrier();  // (the global copy is read by the next launch only)
 }
 
-// Probe logits of the P rows of request `req` at stage d on MFMA: wave w
-// (w < 2) takes probes 16 w .. 16 w + 15 as the 16 tokens of a 16x16 tile
-// (A: their W rows from memory) against the rows' head inputs in nx.u (B),
-// and the same product of absolute values for the margin.  Missing probes
-// get kNegBig.
+// Probe logits of the P rows of request `req` at stage d on MFMA: tile t
+// (t < 2) holds probes 16 t .. 16 t + 15 as the 16 tokens of a 16x16 tile
+// (A: their W rows, staged in nx.pw) against the rows' head inputs in nx.u
+// (B), with the same product of absolute values for the margin; waves 2 g + t
+// (g < kProbeSplit) take every kProbeSplit-th rank chunk of tile t, and the
+// shares are summed.  Two waves per tile measured fastest (eight: their
+// sum costs more; one: a 16-chunk chain per wave).  Missing probes get
+// kNegBig.
 template <int DT>
 __device__ void probe_logits(const Plan& p, int P, NextShared& nx) {
   constexpr int KC = DT ? 32 : 16;  // rank elements per MFMA step
@@ -2325,10 +2328,20 @@ __device__ void probe_logits(const Plan& p, int P, NextShared& nx) {
   // the shares summed (in share order); missing probes get kNegBig
   for (int e = threadIdx.x; e < 2 * kTile * kTile; e += blockDim.x) {
     const int t = e / (kTile * kTile), qi = e / kTile, row = e % kTile;  // qi = 16 t + token
+    float zs[kProbeSplit], as[kProbeSplit];
+#pragma unroll
+    for (int g = 0; g < kProbeSplit; ++g) {
+      const int gg = min(g, ng - 1);
+      zs[g] = nx.pz[(t * kProbeSplit + gg) * kTile * kTile + (qi - t * kTile) * kTile + row];
+      as[g] = nx.pa[(t * kProbeSplit + gg) * kTile * kTile + (qi - t * kTile) * kTile + row];
+    }
     float z = 0.0f, a = 0.0f;
-    for (int g = 0; g < ng; ++g) {
-      z += nx.pz[(t * kProbeSplit + g) * kTile * kTile + (qi - t * kTile) * kTile + row];
-      a += nx.pa[(t * kProbeSplit + g) * kTile * kTile + (qi - t * kTile) * kTile + row];
+#pragma unroll
+    for (int g = 0; g < kProbeSplit; ++g) {
+      if (g < ng) {
+        z += zs[g];
+        a += as[g];
+      }
     }
     if (row < P && qi < np) {
       const bool there = nx.pt[qi] >= 0;
