@@ -75,8 +75,9 @@ pctree_status pctree_debug_set(const pctree_debug_config* cfg);
  *   1  first streaming workgroup of the single-launch round, 2 the last
  *      one: 0 frontier wait begins, 1 head input built, 2 stream done,
  *      3 slice records published
- *   3  per-stage launches, a stage with more than 16 head rows: workgroup 0
- *      of the head kernel: 0 start, 1 stream done, 2 end
+ *   3  per-stage launches, a stage of the wide form (every stage of a round
+ *      whose frontier can exceed 16 rows): workgroup 0 of the head kernel:
+ *      0 start, 1 stream done, 2 end
  *   4  the same stage's merge-and-select workgroup of request 0: 0 start,
  *      1 rows merged, 2 end (selection, next head input and row bounds)
  * Every stage has its row (B <= PCTREE_MAX_BLOCK < PCTREE_TIMELINE_STAGES - 1). */

@@ -450,12 +450,19 @@ __device__ void init_request(const Plan& p, int req, int tid, int nth) {
   init_request_body(p, req, tid, nth);
 }
 
-// Head rows per request of stage d, and whether stage d runs the wide form.
+// Head rows per request of stage d, and whether stage d of a per-stage-launch
+// round runs the wide form: when it has more than 16 head rows, and in every
+// stage of a round whose frontier can exceed 16 rows (the stages with fewer
+// rows then also take the bounded head stream and the one merge-and-select
+// launch: 900 -> 893 us per round at 8 requests with k' = 16, and 867 -> 820
+// and 849 -> 794 us in the two control scorings, whose stages all have one
+// row per request).  Rounds with at most 16 frontier rows launched per stage
+// keep the narrow form.
 __device__ __host__ __forceinline__ int head_rows(int mode, int d, int kk) {
   return (d == 0 || mode != 0) ? 1 : kk;
 }
 __device__ __host__ __forceinline__ bool stage_wide(int mode, int d, int R, int kk) {
-  return R * head_rows(mode, d, kk) > kNarrowRows;
+  return R * head_rows(mode, d, kk) > kNarrowRows || R * kk > kNarrowRows;
 }
 
 // ---------------------------------------------------------------------------

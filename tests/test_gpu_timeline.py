@@ -62,7 +62,7 @@ def test_timeline_build_keeps_the_tree(tmp_path, label, args, w):
                 assert v is not None and v >= 0.0, (label, s["stage"], key, v)
         assert res["stage_period_us"] > 0.0 and res["round_us"] > res["emission_us"] > 0.0
     else:
-        assert len(stages) == w.B - 1  # the wide stages: every stage but the first
+        assert len(stages) == w.B  # more than 16 frontier rows: every stage is wide
         for s in stages:
             for key in ("head_stream_us", "head_us", "head_to_merge_us", "merge_rows_us",
                         "merge_select_us"):

@@ -52,7 +52,7 @@ def test_summary_of_a_single_launch_round():
 
 def test_summary_of_per_stage_launches():
     t = _stamps()
-    for d in (1, 2, 3):  # wide stages only: stage 0 has its own kernels
+    for d in (1, 2, 3):  # (stage 0 left unstamped: a stage of the narrow form)
         t[T.HEAD, d, :3] = 60.0 * d + np.array([0.0, 30.0, 35.0])
         t[T.MERGE, d, :3] = 60.0 * d + np.array([37.0, 44.0, 55.0])
     r = T.summarize(t, 4)
