@@ -2059,8 +2059,13 @@ __device__ __forceinline__ uint64_t probe_scan(const Plan& p, size_t base) {
     const uint64_t c = probe_key(load_elem<DT>(p.L, base + v), v);
     k = c > k ? c : k;
   }
+  // the aligned body: the thread's best logit and its token, compared as
+  // floats in increasing token order (a strict comparison keeps the lowest
+  // token of equal logits, as the key order does; -0 equals +0 in both)
   const u32x4* vec = (const u32x4*)((const char*)p.L + (base + head) * ES);
   constexpr int kBatch = 8;  // loads issued before any is used
+  float bz = -INFINITY;
+  int bv = -1;
   for (int c0 = 0; c0 < nvec; c0 += kBatch * kProbeThreads) {
     u32x4 w[kBatch];
 #pragma unroll
@@ -2074,12 +2079,16 @@ __device__ __forceinline__ uint64_t probe_scan(const Plan& p, size_t base) {
           const uint32_t word = w[b][e * ES / 4];
           const float z = DT ? __uint_as_float((e & 1) ? (word & 0xffff0000u) : (word << 16))
                              : __uint_as_float(word);
-          const int v = head + c * PER + e;
-          const uint64_t key = probe_key(z, v);
-          k = key > k ? key : k;
+          const bool up = z > bz || bv < 0;
+          bz = up ? z : bz;
+          bv = up ? head + c * PER + e : bv;
         }
       }
     }
+  }
+  if (bv >= 0) {
+    const uint64_t key = probe_key(bz, bv);
+    k = key > k ? key : k;
   }
   return k;
 }
