@@ -135,6 +135,8 @@ SHAPES = [
     (33, 3, 20, 6, 32, 20, "bf16"),    # 20 requests: wide from stage 0; ragged last tile
     (500, 2, 16, 16, 32, 256, "bf16"),  # the request limit: 4096 rows, 32 column groups
     (9000, 3, 64, 16, 512, 3, "bf16"),  # the largest rank
+    (7, 3, 20, 8, 32, 4, "bf16"),      # a vocabulary under one super-tile: k' = 7, 7 probes
+    (7, 3, 20, 8, 16, 4, "f32"),       # the same in fp32
 ]
 
 
