@@ -2409,8 +2409,10 @@ __device__ void row_bounds(const Plan& p, int d, int P, int req, NextShared& nx)
 }
 
 // Multi-launch form: request state in the workspace, the stage-0 head input
-// and, when stage 0 runs the wide form, its rows' bounds.
-__global__ __launch_bounds__(kEmitThreads) void prologue_kernel(Plan p) {
+// and, when stage 0 runs the wide form, its rows' bounds.  One workgroup
+// per request, 16 waves like the merge-and-select workgroups (4 waves made
+// the stage-0 bounds 5 us slower per round at 8 requests).
+__global__ __launch_bounds__(kSelectThreads) void prologue_kernel(Plan p) {
   __shared__ NextShared nx;
   __shared__ int toks[1];
   const int req = blockIdx.x;
@@ -3363,7 +3365,7 @@ hipError_t launch_round(const Plan& p0, hipStream_t st) {
   for (int d = 0; d < p.B; ++d) any_wide = any_wide || stage_wide(p.mode, d, p.R, p.kk);
   if (any_wide && !p.unbounded)
     hipLaunchKernelGGL(probe_kernel, dim3(p.R * p.B), dim3(kProbeThreads), 0, st, p);
-  hipLaunchKernelGGL(prologue_kernel, dim3(p.R), dim3(kEmitThreads), 0, st, p);
+  hipLaunchKernelGGL(prologue_kernel, dim3(p.R), dim3(kSelectThreads), 0, st, p);
   const StageFn head = head_fn(p);
   const StageFn sel = select_fn(p.kmax);
   const StageFn head_thr = any_wide ? head_thr_fn(p) : nullptr;
