@@ -1272,6 +1272,20 @@ __device__ __forceinline__ int count_greater(const uint64_t* keys, int n, uint64
   return cnt;
 }
 
+// The number of keys[0..n) greater than `key` when keys are sorted in
+// descending order: a binary search, log2(n) dependent reads instead of n.
+__device__ __forceinline__ int count_greater_desc(const uint64_t* keys, int n, uint64_t key) {
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (keys[mid] > key)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  return lo;
+}
+
 // The same count by a group of T adjacent lanes (T a power of two <= 64):
 // lane q of the group counts keys q, q + T, q + 2T, ... (the group reads T
 // consecutive keys per load, no bank conflicts), eight loads in flight at a
@@ -1481,7 +1495,7 @@ __device__ __forceinline__ void stage_select_body(const Plan& p, const State& st
     if (tid < ns) {
       const int c = prune ? sh.sci[s0 + tid] : s0 + tid;
       key = keys[s0 + tid];
-      pos = sh.rank[c] + count_greater(sh.tkey, ncur, key);
+      pos = sh.rank[c] + count_greater_desc(sh.tkey, ncur, key);  // (the top-N is sorted)
       node = nbase + c - rq * per_req;
     } else if (tid >= 256 && tid < 256 + ncur) {
       const int i = tid - 256;
