@@ -3029,7 +3029,8 @@ __global__ __launch_bounds__(kWideWaves * 64) void head_thr_kernel(Plan p, int d
   __syncthreads();
   const int nov = ovl[kThrRows];
   if (nov > 0)
-    thr_exact<DT, NCMAX, KMAX>(p, d, P, slice, t0, t1, ovl, nov, (uint64_t*)ring0);  if (blockIdx.x == 0) TIMELINE_STAMP(3, d, 2);
+    thr_exact<DT, NCMAX, KMAX>(p, d, P, slice, t0, t1, ovl, nov, (uint64_t*)ring0);
+  if (blockIdx.x == 0) TIMELINE_STAMP(3, d, 2);
 }
 
 // One WG per request after a wide head stage: each of its rows (one wave per
