@@ -83,6 +83,21 @@ def test_shared_batched_serving(req):
     say(f"[modes] shared {w.name} request {req}: {reps}")
 
 
+@pytest.mark.parametrize("req", range(CONFIGS["qwen14b_b16_r8"].R))
+def test_independent_batched_serving(req):
+    """Eight requests, k = 16, N = 128, r = 512, parent-independent scoring
+    (every stage in the wide form with one row per request): one GPU call,
+    every request replayed against the oracle."""
+    w = CONFIGS["qwen14b_b16_r8"]
+    if "independent" not in _CACHE:
+        say(f"[modes] independent {w.name}")
+        inp = _CACHE["shared"][0] if "shared" in _CACHE else make_inputs(w)
+        _CACHE["independent"] = (inp, run(inp, w.k, w.N, "independent"))
+    inp, out = _CACHE["independent"]
+    reps = C.compare_batch(out, inp, w.k, w.N, requests=[req], mode="independent")
+    say(f"[modes] independent {w.name} request {req}: {reps}")
+
+
 def test_modes_differ_under_conditioning():
     """sigma_E = 1: the three scorings give three different trees, and the
     GPU's tree of each control mode passes the comparator for that mode."""
